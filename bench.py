@@ -2,12 +2,16 @@
 
 One step = the MXFP4 backward pass (RHT + stochastic-rounding quantisation of
 all four operands, two scaled MXFP4 GEMMs, 16/9g rescale) of every linear layer
-of a GPT-345M-shaped transformer block: 4096 tokens, hidden 1024, linears QKV
-1024->3072, proj 1024->1024, fc1 1024->4096, fc2 4096->1024, g = 64. Inputs are
-seeded synthetic tensors of those shapes (workloads.CONFIGS["gpt345m"]),
-resident in HBM before the timed region. Consecutive steps rotate through
-copies of the inputs held in distinct buffers, at least 512 MB in all, so the
-256 MB MALL cannot serve a step's inputs from the step before.
+of one transformer block. The headline workload is the GPT-6.7B-shaped block:
+16384 tokens, hidden 4096, linears QKV 4096->12288, proj 4096->4096, fc1
+4096->16384, fc2 16384->4096 (13.19 TFLOP of backward GEMMs per step), g = 64,
+dY heavy-tailed with 0.5% of its 32-element blocks scaled x1000
+(workloads.CONFIGS["gpt6.7b"]); --config picks another block. The GPT-345M
+block (4096 tokens, hidden 1024) is timed the same way as a secondary figure.
+Inputs are seeded synthetic tensors, resident in HBM before the timed region.
+Consecutive steps rotate through copies of the inputs held in distinct
+buffers, at least 512 MB in all, so the 256 MB MALL cannot serve a step's
+inputs from the step before (one GPT-6.7B input set is 2.4 GB on its own).
 
 Printed: ONE JSON line with the contract fields, plus
 * roofline: the kernel with the largest share of the step, timed per launch
@@ -39,7 +43,8 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-CONFIG = "gpt345m"
+DEFAULT_CONFIG = "gpt6.7b"
+SECONDARY_CONFIG = "gpt345m"
 METRIC = "MXFP4 backward-GEMM TFLOP/s incl. RHT+SR quantize; quantize GB/s; % of peak"
 HBM_PEAK_GBS = 8000.0
 MXFP4_PEAK_TFLOPS = 10100.0
@@ -51,8 +56,9 @@ QUANT_BYTES_PER_ELEM = 2.0 + 0.5 + 1.0 / 32.0     # bf16 in, two codes per byte,
 SEED = 0x0345_0000_0000_0000
 # HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE passes of
 # this benchmark (scaled by a copy of known size), with the hash of the kernel
-# sources they were measured on.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_gpt345m.json")
+# sources they were measured on; one file per workload.
+def traffic_file(config):
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_{config}.json")
 
 
 def kernel_source_hash():
@@ -66,12 +72,12 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_counter(kernel, key):
+def measured_counter(config, kernel, key):
     """A per-launch counter figure of `kernel` (`hbm_bytes_per_launch`,
-    `valu_insts_per_launch`) from the committed counter summary, or None if
-    there is none or the kernels have changed since it was taken."""
+    `valu_insts_per_launch`) from the committed counter summary of `config`, or
+    None if there is none or the kernels have changed since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(traffic_file(config)) as fh:
             d = json.load(fh)
     except (OSError, ValueError):
         return None
@@ -81,13 +87,17 @@ def measured_counter(kernel, key):
     return None if k is None else k.get(key)
 
 
-def measured_traffic(kernel):
-    return measured_counter(kernel, "hbm_bytes_per_launch")
+def measured_traffic(config, kernel):
+    return measured_counter(config, kernel, "hbm_bytes_per_launch")
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=["gpt6.7b", "gpt1.3b", "gpt345m", "tiny"],
+                    help="block whose backward is the headline step (default %(default)s)")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the secondary GPT-345M step timing")
     ap.add_argument("--steps", type=int, default=100)
     # Default warm-up: as many steps as fill WARMUP_S seconds (at least 20). The
     # GPU's clocks take about half a second of load to settle: with 20 warm-up
@@ -104,7 +114,7 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step: standalone quantiser and GEMM throughput sweep")
     ap.add_argument("--write-traffic", nargs="+", metavar="CSV",
-                    help="write profiles/hbm_traffic_gpt345m.json from the counter_collection.csv files of a "
+                    help="write profiles/hbm_traffic_<config>.json from the counter_collection.csv files of a "
                          "rocprofv3 --pmc FETCH_SIZE run and a --pmc WRITE_SIZE run of this benchmark with "
                          "--calib-copy, then exit")
     ap.add_argument("--rht-overhead", action="store_true",
@@ -373,58 +383,98 @@ def gemm_baselines(torch, layers, reps=10):
     return out
 
 
-def cpu_baseline(budget_s):
-    """Time the CPU oracle on a bounded sample of the step and scale to TFLOP/s.
-
-    Sample: for each linear, the oracle quantises whole rows of each of the four
-    operands (quantisation is row-local, so a row sample is exact work) and
-    computes sampled output rows of both GEMMs in FP64. Per-element quantise
-    time and per-FLOP GEMM time are measured separately and the full step time
-    is their sum over the step's element and FLOP counts."""
-    import oracle
-    import workloads
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = 1
-    cfg = workloads.CONFIGS[CONFIG]
-    t = cfg["tokens"]
+        return 1
+
+
+def cpu_oracle_full(config, linears=None):
+    """The oracle's Algorithm 3 (oracle.linear_backward: all four operands
+    quantised whole, both GEMMs in FP64) timed in full on the named linears of a
+    config (all of them by default)."""
+    import oracle
+    import workloads
+    cfg = workloads.CONFIGS[config]
+    t, g = cfg["tokens"], cfg["g"][0]
+    secs, flops, elems, names = 0.0, 0, 0, []
+    for name, fin, fout in cfg["linears"]:
+        if linears and name not in linears:
+            continue
+        dy, x, w = workloads.linear_inputs(config, name)
+        t0 = time.perf_counter()
+        oracle.linear_backward(dy, x, w, g, SEED)
+        secs += time.perf_counter() - t0
+        flops += 4 * t * fin * fout
+        elems += 2 * t * fout + fin * fout + fin * t
+        names.append(name)
+    return {"config": config, "linears": names, "seconds": secs, "gemm_flops": flops, "quant_elems": elems,
+            "value": flops / secs / 1e12, "unit": "TFLOP/s"}
+
+
+def cpu_baseline(config, budget_s):
+    """The CPU oracle timed on the GPU machine's host cores.
+
+    * In full: the tiny single-linear config (256 tokens, 256 x 256) and the
+      QKV linear of the GPT-345M block.
+    * Sampled, for the headline block (whose oracle step runs for most of an
+      hour): per linear, the oracle quantises whole rows of each of the four
+      operands -- the first 64 logical rows of dY and dY^T, the first 256 of W^T
+      and x^T (quantisation is row-local, so a row sample is exact work) -- and
+      multiplies the sampled rows of both GEMMs in FP64. The step time is the
+      measured per-element quantise time times the step's elements plus the
+      measured per-FLOP GEMM time times its FLOPs. The skinny sampled GEMMs run
+      BLAS below its full-size rate, so this estimate errs towards a slower
+      oracle."""
+    import oracle
+    import workloads
+    threads = _blas_threads()
+    full = {"tiny": cpu_oracle_full("tiny"), "gpt345m_qkv": cpu_oracle_full("gpt345m", ["qkv"])}
+    cfg = workloads.CONFIGS[config]
+    t, g = cfg["tokens"], cfg["g"][0]
     q_elems_total, flops_total = 0, 0
     q_time, q_elems, g_time, g_flops = 0.0, 0, 0.0, 0
     start = time.perf_counter()
-    rows_q, rows_g = 64, 16
-    for li, (name, fin, fout) in enumerate(cfg["linears"]):
-        dy, x, w = workloads.linear_inputs(CONFIG, name)
+    rows_a, rows_b = 64, 256
+    sampled = []
+    for name, fin, fout in cfg["linears"]:
         q_elems_total += 2 * t * fout + fin * fout + fin * t
         flops_total += 4 * t * fin * fout
         if time.perf_counter() - start > budget_s:
             continue
-        ops = [(dy, 0), (np.ascontiguousarray(w.T), 1), (np.ascontiguousarray(dy.T), 2),
-               (np.ascontiguousarray(x.T), 3)]
+        dy, x, w = workloads.linear_inputs(config, name)
+        # Logical rows of the four operands: dY [T, out], W^T [in, out],
+        # dY^T [out, T], x^T [in, T]; a row of a transposed operand is a column
+        # of the stored matrix.
+        ops = [(dy[:rows_a], 0), (np.ascontiguousarray(w[:, :rows_b].T), 1),
+               (np.ascontiguousarray(dy[:, :rows_a].T), 2), (np.ascontiguousarray(x[:, :rows_b].T), 3)]
         qs = []
         for bits, i in ops:
-            ids = np.arange(min(rows_q, bits.shape[0]))
+            ids = np.arange(bits.shape[0])
             t0 = time.perf_counter()
-            qs.append(oracle.quantize_rht_sr(bits[ids], 64, SEED ^ i, row_ids=ids))
+            qs.append(oracle.quantize_rht_sr(bits, g, SEED ^ i, row_ids=ids))
             q_time += time.perf_counter() - t0
-            q_elems += len(ids) * bits.shape[1]
-        # GEMM sample: rows_g output rows of dX and dW against full B operands
-        # (B quantisation is not timed again; its cost is in the per-element rate).
-        for a, b in ((qs[0], oracle.quantize_rht_sr(np.ascontiguousarray(w.T), 64, SEED ^ 1)),
-                     (qs[2], oracle.quantize_rht_sr(np.ascontiguousarray(x.T), 64, SEED ^ 3))):
+            q_elems += bits.size
+        for a, b in ((qs[0], qs[1]), (qs[2], qs[3])):
             t0 = time.perf_counter()
-            oracle.gemm_f64(a[0][:rows_g], a[1][:rows_g], b[0], b[1])
+            oracle.gemm_f64(a[0], a[1], b[0], b[1])
             g_time += time.perf_counter() - t0
-            g_flops += 2 * rows_g * b[0].shape[0] * b[0].shape[1]
+            g_flops += 2 * a[0].shape[0] * b[0].shape[0] * a[0].shape[1]
+        sampled.append(name)
     est_s = q_elems_total * (q_time / q_elems) + flops_total * (g_time / g_flops)
     return {
         "value": flops_total / est_s / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
         "host_cpus": os.cpu_count(),
-        "sample": (f"oracle on {q_elems} quantised elements (first {rows_q} rows of each operand of each "
-                   f"linear) and {g_flops:.3g} FP64 GEMM FLOPs ({rows_g} output rows per GEMM); "
-                   f"step time extrapolated per element / per FLOP: {est_s:.1f} s for the full step"),
-        "quant_elems_per_s": q_elems / q_time, "gemm_flops_per_s": g_flops / g_time,
+        "sample": (f"{config} block step, sampled: the oracle quantised {q_elems} elements (whole logical rows: "
+                   f"the first {rows_a} of dY and dY^T, the first {rows_b} of W^T and x^T, of the linears "
+                   f"{', '.join(sampled)}) and ran {g_flops:.3g} FLOPs of the FP64 GEMMs on those rows; step time "
+                   f"= per-element quantise time x {q_elems_total} elements + per-FLOP GEMM time x "
+                   f"{flops_total:.4g} FLOPs = {est_s:.0f} s. Quantiser single-threaded numpy, GEMM BLAS on "
+                   f"{threads} threads"),
+        "quant_elems_per_s": q_elems / q_time, "gemm_flops_per_s": g_flops / g_time, "est_step_s": est_s,
+        "full_runs": full,
     }
 
 
@@ -558,33 +608,43 @@ def config_runs(torch, mx, steps=10, warmup=3):
     return out
 
 
-def write_traffic(fetch_csv, write_csv, sq_csv=None):
+KERNEL_TAGS = (("quant_kernel<64", "quant_g64"), ("gemm_ring_kernel<128", "gemm_128x128r"),
+               ("gemm_ring_kernel<256", "gemm_256x256"), ("gemm_f4_kernel", "gemm_128x128"),
+               ("reduce_splits", "splitk_reduce"), ("colsum_reduce", "colsum_reduce"))
+
+
+def _kernel_key(name):
+    for tag, short in KERNEL_TAGS:
+        if tag in name:
+            return short
+    return None
+
+
+def write_traffic(config, fetch_csv, write_csv, *sq_csvs):
     """HBM bytes per launch of each library kernel from two rocprofv3 counter
     passes. Each counter is scaled by the ratio of the true bytes of the plain
     256 MiB device copy that --calib-copy appends to what the counter reads for
-    that copy (FETCH_SIZE and WRITE_SIZE are in KiB). With a third pass holding
-    SQ_INSTS_VALU, also the VALU wavefront instructions per launch."""
+    that copy (FETCH_SIZE and WRITE_SIZE are in KiB). Further passes (SQ / GRBM
+    counters such as SQ_INSTS_VALU, SQ_INSTS_MFMA, SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_BUSY_CYCLES, GRBM_GUI_ACTIVE) are averaged per launch as they are."""
     import csv
     copy_bytes = float(1 << 28)
 
-    def per_kernel(path, counter, need_copy=True):
+    def per_kernel(path, counter=None, need_copy=True):
         sums, counts, copy = {}, {}, []
         for r in csv.DictReader(open(path)):
-            if r["Counter_Name"] != counter:
+            if counter is not None and r["Counter_Name"] != counter:
                 continue
             name, v = r["Kernel_Name"], float(r["Counter_Value"])
             if "copyBuffer" in name:
                 copy.append(v)
                 continue
-            key = None
-            for tag, short in (("quant_kernel<64", "quant_g64"), ("gemm_ring_kernel<128", "gemm_128x128r"),
-                               ("gemm_ring_kernel<256", "gemm_256x256"), ("gemm_f4_kernel", "gemm_128x128"),
-                               ("reduce_splits", "splitk_reduce")):
-                if tag in name:
-                    key = short
+            key = _kernel_key(name)
             if key:
-                sums[key] = sums.get(key, 0.0) + v
-                counts[key] = counts.get(key, 0) + 1
+                k2 = key if counter is not None else (key, r["Counter_Name"])
+                # one row per dispatch and counter
+                sums[k2] = sums.get(k2, 0.0) + v
+                counts[k2] = counts.get(k2, 0) + 1
         if not need_copy:
             return {k: (sums[k] / counts[k], counts[k]) for k in sums}, 1.0
         if not copy:
@@ -599,23 +659,94 @@ def write_traffic(fetch_csv, write_csv, sq_csv=None):
         kernels[k] = {"launches_counted": fetch[k][1], "fetch_kib_per_launch": fetch[k][0],
                       "write_kib_per_launch": write[k][0],
                       "hbm_bytes_per_launch": (fetch[k][0] * fscale + write[k][0] * wscale) * 1024.0}
-    if sq_csv:
-        valu, _ = per_kernel(sq_csv, "SQ_INSTS_VALU", need_copy=False)
-        for k in kernels:
-            if k in valu:
-                kernels[k]["valu_insts_per_launch"] = valu[k][0]
-    d = {"source_hash": kernel_source_hash(), "fetch_scale": fscale, "write_scale": wscale, "kernels": kernels}
-    with open(TRAFFIC_FILE, "w") as fh:
+    for path in sq_csvs:
+        extra, _ = per_kernel(path, None, need_copy=False)
+        for (k, cname), (v, _n) in extra.items():
+            if k in kernels:
+                kernels[k].setdefault("counters_per_launch", {})[cname] = v
+                if cname == "SQ_INSTS_VALU":
+                    kernels[k]["valu_insts_per_launch"] = v
+    d = {"config": config, "source_hash": kernel_source_hash(), "fetch_scale": fscale, "write_scale": wscale,
+         "kernels": kernels}
+    with open(traffic_file(config), "w") as fh:
         json.dump(d, fh, indent=1)
     print(json.dumps(d, indent=1))
+
+
+def load_layers(torch, config):
+    import workloads
+    cfg = workloads.CONFIGS[config]
+    layers = [Layer(torch, name, fin, fout, *workloads.linear_inputs(config, name))
+              for name, fin, fout in cfg["linears"]]
+    torch.cuda.synchronize()
+    return cfg, layers
+
+
+def traced(torch, mx, sets, g, steps):
+    """Per-kernel times of `steps` steps from the library's kernel tracing (HIP
+    events recorded on each launch's own stream)."""
+    mx.mx_profile_start()
+    for i in range(steps):
+        step(mx, sets[i % len(sets)], g)
+    torch.cuda.synchronize()
+    prof = mx.mx_profile_stop()
+    kernels = {}
+    for name, st in prof.items():
+        d = {"ms_per_step": st["total_ms"] / steps, "launches_per_step": st["launches"] / steps,
+             "avg_us": st["total_ms"] * 1e3 / st["launches"]}
+        if st["work_is_flops"]:
+            d["tflops"] = st["work"] / (st["total_ms"] * 1e-3) / 1e12
+        else:
+            d["gbs"] = st["work"] / (st["total_ms"] * 1e-3) / 1e9
+        kernels[name] = d
+    return prof, kernels
+
+
+def roofline_of(config, prof, kernel, steps):
+    """Roofline entry of one traced kernel: its algorithmic work per launch over
+    its average launch time, against the MXFP4 MFMA peak (FLOP work) or HBM
+    (byte work); traffic from the committed counter summary when its kernel
+    sources are current."""
+    st = prof[kernel]
+    secs = st["total_ms"] * 1e-3
+    if st["work_is_flops"]:
+        achieved = st["work"] / secs / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MXFP4_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / MXFP4_PEAK_TFLOPS}
+    else:
+        achieved = st["work"] / secs / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof["traffic"] = measured_traffic(config, kernel)
+    roof.update({"kernel": kernel, "launches_per_step": st["launches"] / steps,
+                 "avg_us": st["total_ms"] * 1e3 / st["launches"], "per_launch": st["work"] / st["launches"],
+                 "work_unit": "FLOP" if st["work_is_flops"] else "byte"})
+    return roof
+
+
+def alu_roofline_of(config, prof, kernel):
+    """The quantiser is bound by vector ALU issue, not HBM: its counted VALU
+    wavefront instructions (64 lanes each) per launch over the launch time,
+    against the VALU issue peak (None without a current counter summary)."""
+    valu = measured_counter(config, kernel, "valu_insts_per_launch")
+    if valu is None or kernel not in prof:
+        return None
+    st = prof[kernel]
+    avg_s = st["total_ms"] * 1e-3 / st["launches"]
+    lane_ops = valu * 64.0
+    r = {"bound": "alu", "kernel": kernel, "achieved": lane_ops / avg_s, "peak": VALU_PEAK_LANE_OPS,
+         "unit": "lane-op/s", "frac": lane_ops / avg_s / VALU_PEAK_LANE_OPS, "lane_ops_per_launch": lane_ops}
+    if not st["work_is_flops"]:
+        r["lane_ops_per_element"] = lane_ops / (st["work"] / st["launches"] / QUANT_BYTES_PER_ELEM)
+    return r
 
 
 def main():
     args = parse()
     if args.write_traffic:
-        if len(args.write_traffic) not in (2, 3):
-            raise SystemExit("--write-traffic FETCH_CSV WRITE_CSV [SQ_CSV]")
-        write_traffic(*args.write_traffic)
+        if len(args.write_traffic) < 2:
+            raise SystemExit("--write-traffic FETCH_CSV WRITE_CSV [COUNTER_CSV ...]")
+        write_traffic(args.config, *args.write_traffic)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
@@ -637,14 +768,11 @@ def main():
     if args.rht_overhead:
         print(json.dumps({"rht_overhead": rht_overhead(torch, mx)}))
         return
-    cfg = workloads.CONFIGS[CONFIG]
+    config = args.config
+    t0 = time.perf_counter()
+    cfg, layers = load_layers(torch, config)
     g = cfg["g"][0]
-    layers = []
-    for name, fin, fout in cfg["linears"]:
-        dy, x, w = workloads.linear_inputs(CONFIG, name)
-        layers.append(Layer(torch, name, fin, fout, dy, x, w))
-    torch.cuda.synchronize()
-    print(f"[bench] inputs ready ({CONFIG})", file=sys.stderr, flush=True)
+    print(f"[bench] inputs ready ({config}, {time.perf_counter() - t0:.1f} s)", file=sys.stderr, flush=True)
 
     sets, set_bytes = input_sets(layers)
     if args.warmup is None:
@@ -657,6 +785,7 @@ def main():
     # Events between consecutive steps give the per-step spread; the value is
     # the whole timed region over the number of steps.
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
     t_wall = time.perf_counter()
     ev[0].record()
     for i in range(args.steps):
@@ -669,64 +798,32 @@ def main():
     pct = lambda q: step_times[min(len(step_times) - 1, int(q * len(step_times)))]
     flops = sum(L.flops() for L in layers)
     value = flops / (ms * 1e-3) / 1e12
-    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step, {value:.0f} TFLOP/s", file=sys.stderr, flush=True)
 
-    # Second timed pass with the library's kernel tracing on: HIP events around
-    # each of its launches, on the stream the launch uses.
-    mx.mx_profile_start()
-    for i in range(args.steps):
-        step(mx, sets[i % len(sets)], g)
-    torch.cuda.synchronize()
-    prof = mx.mx_profile_stop()
-    kernels = {}
-    for name, st in prof.items():
-        per_step = st["total_ms"] / args.steps
-        d = {"ms_per_step": per_step, "launches_per_step": st["launches"] / args.steps,
-             "avg_us": st["total_ms"] * 1e3 / st["launches"]}
-        if st["work_is_flops"]:
-            d["tflops"] = st["work"] / (st["total_ms"] * 1e-3) / 1e12
-        else:
-            d["gbs"] = st["work"] / (st["total_ms"] * 1e-3) / 1e9
-        kernels[name] = d
+    # Second pass of the same steps with the library's kernel tracing on.
+    prof, kernels = traced(torch, mx, sets, g, args.steps)
     dom = max(prof, key=lambda k: prof[k]["total_ms"])
-    st = prof[dom]
-    if st["work_is_flops"]:
-        achieved = st["work"] / (st["total_ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": MXFP4_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / MXFP4_PEAK_TFLOPS, "traffic": None}
-    else:
-        achieved = st["work"] / (st["total_ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": None}
-    roof["traffic"] = measured_traffic(dom)
-    # The quantiser is bound by vector ALU issue, not HBM: its counted VALU
-    # wavefront instructions (64 lanes each) per launch over the launch time,
-    # against the VALU issue peak.
-    valu = measured_counter(dom, "valu_insts_per_launch")
-    alu_roof = None
-    if valu is not None:
-        avg_s = st["total_ms"] * 1e-3 / st["launches"]
-        lane_ops = valu * 64.0
-        alu_roof = {"bound": "alu", "kernel": dom, "achieved": lane_ops / avg_s, "peak": VALU_PEAK_LANE_OPS,
-                    "unit": "lane-op/s", "frac": lane_ops / avg_s / VALU_PEAK_LANE_OPS,
-                    "lane_ops_per_launch": lane_ops}
-        if not st["work_is_flops"]:
-            alu_roof["lane_ops_per_element"] = lane_ops / (st["work"] / st["launches"] / QUANT_BYTES_PER_ELEM)
-    roof.update({"kernel": dom, "launches_per_step": st["launches"] / args.steps,
-                 "avg_us": st["total_ms"] * 1e3 / st["launches"], "per_launch": st["work"] / st["launches"]})
+    roof = roofline_of(config, prof, dom, args.steps)
     quant_ms = sum(v["total_ms"] for k, v in prof.items() if k.startswith("quant"))
     quant_bytes = sum(v["work"] for k, v in prof.items() if k.startswith("quant"))
+    gemm_ms = sum(v["total_ms"] for k, v in prof.items() if k.startswith("gemm") or k == "splitk_reduce")
+    qk = max((k for k in prof if k.startswith("quant")), key=lambda k: prof[k]["total_ms"], default=None)
+    hidden = {"gpt6.7b": 4096, "gpt1.3b": 2048, "gpt345m": 1024, "tiny": 256}[config]
     res = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "mxfp4", "data": "synthetic",
-        "config": {"workload": "gpt345m_block_backward", "tokens": cfg["tokens"], "hidden": 1024,
+        "config": {"workload": f"{config}_block_backward", "tokens": cfg["tokens"], "hidden": hidden,
                    "linears": [[n_, i_, o_] for n_, i_, o_ in cfg["linears"]], "g": g,
-                   "parallelism": "none"},
+                   "gemm_flops_per_step": flops, "parallelism": "none"},
         "quantize_gbs": quant_bytes / (quant_ms * 1e-3) / 1e9,
+        "quantize_ms_per_step": quant_ms / args.steps,
+        "gemm_ms_per_step": gemm_ms / args.steps,
+        "gemm_tflops": flops / (gemm_ms * 1e-3) / 1e12,
         "mfma_peak_frac": value / MXFP4_PEAK_TFLOPS,
         "roofline": roof,
-        "alu_roofline": alu_roof,
+        "quantize_roofline": roofline_of(config, prof, qk, args.steps) if qk else None,
+        "alu_roofline": alu_roofline_of(config, prof, qk) if qk else None,
         "kernels": kernels,
         "kernel_source_hash": kernel_source_hash(),
         "wall_s_timed": t_wall,
@@ -746,9 +843,40 @@ def main():
     if not args.no_baselines:
         print("[bench] bf16 / fp8 baselines", file=sys.stderr, flush=True)
         res["baselines"] = gemm_baselines(torch, layers)
+        res["speedups"] = {f"vs_{k}": v["ms_per_step"] / ms for k, v in res["baselines"].items()
+                           if "ms_per_step" in v}
+    del sets, layers
+    torch.cuda.empty_cache()
+    if not args.no_secondary and config != SECONDARY_CONFIG:
+        # The GPT-345M block, timed the same way (its GEMMs are bound by their
+        # FP32 output writes, its quantiser launches are short).
+        cfg2, layers2 = load_layers(torch, SECONDARY_CONFIG)
+        sets2, _ = input_sets(layers2)
+        warm_up(torch, lambda i: step(mx, sets2[i % len(sets2)], cfg2["g"][0]), seconds=0.25)
+        n2 = max(args.steps, 50)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n2):
+            step(mx, sets2[i % len(sets2)], cfg2["g"][0])
+        e1.record()
+        torch.cuda.synchronize()
+        ms2 = e0.elapsed_time(e1) / n2
+        flops2 = sum(L.flops() for L in layers2)
+        prof2, kern2 = traced(torch, mx, sets2, cfg2["g"][0], n2)
+        sec = {"workload": f"{SECONDARY_CONFIG}_block_backward", "steps": n2, "ms_per_step": ms2,
+               "tflops": flops2 / (ms2 * 1e-3) / 1e12, "kernels": kern2}
+        if not args.no_baselines:
+            sec["baselines"] = gemm_baselines(torch, layers2)
+            sec["speedups"] = {f"vs_{k}": v["ms_per_step"] / ms2 for k, v in sec["baselines"].items()
+                               if "ms_per_step" in v}
+        res["secondary"] = sec
+        print(f"[bench] secondary {SECONDARY_CONFIG}: {ms2:.4f} ms/step", file=sys.stderr, flush=True)
+        del sets2, layers2
+        torch.cuda.empty_cache()
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(config, args.cpu_budget)
     print(json.dumps(res))
 
 

@@ -25,6 +25,11 @@
  * - A call with an empty problem (a zero dimension) enqueues nothing and
  *   returns MX_OK; its pointers may then be NULL.
  * - Outputs are fully overwritten. Calls are thread-safe.
+ * - Graph capture: every call that enqueues work first asks whether `stream`
+ *   is being captured into a HIP graph and, if so, returns MX_ERR_CAPTURE and
+ *   enqueues nothing (these calls may allocate or free their workspace in
+ *   stream order, which a graph cannot replay; a graph would also keep a
+ *   workspace address that a later call may free).
  * - Only gfx950 devices are supported (MX_ERR_DEVICE otherwise).
  *
  * The quantised format (MXFP4)
@@ -42,8 +47,9 @@
  * ----------------------------------------------------------
  * 1. Sign flip and Hadamard, per g-block of g consecutive elements
  *    (g in {32, 64, 128, 256}, cols % g == 0): y = H_g (S o x) with H_g the
- *    +-1 Sylvester matrix (Eq. hadrec without its scale factor; H H^T = g I)
- *    and S in {+-1}^g shared by every block. In FP32, evaluated by the
+ *    +-1 Sylvester matrix (the Hadamard recursion of Sec. 3.2 without its
+ *    scale factor; H H^T = g I) and S in {+-1}^g shared by every block.
+ *    In FP32, evaluated by the
  *    Sylvester recursion: the two half-size transforms first, then their sum
  *    and difference; IEEE round-to-nearest-even, no FMA, subnormals kept.
  * 2. Per 32-element block of y: E = floor(log2 max|y|) - 2 + 127 (shared_exp
@@ -84,7 +90,8 @@ enum mx_status {
   MX_ERR_NOMEM = -6,   /* workspace allocation failed */
   MX_ERR_DEVICE = -7,  /* the current device is not a gfx950 GPU */
   MX_ERR_MODE = -8,    /* mode is not one of MX_MODE_* */
-  MX_ERR_FLAGS = -9    /* flags holds a bit that is not one of MX_BWD_* */
+  MX_ERR_FLAGS = -9,   /* flags holds a bit that is not one of MX_BWD_* */
+  MX_ERR_CAPTURE = -10 /* the stream is being captured into a graph */
 };
 
 /*
@@ -180,8 +187,8 @@ int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B
  * stream. A call that needs more than the workspace holds grows it in stream
  * order (the old block is freed after the work already enqueued on `stream`,
  * the new one allocated from a pool the library owns); the workspace is held
- * until the process ends. Because a call may allocate, calls cannot be
- * captured into a HIP graph.
+ * until the process ends. Because a call may allocate, it refuses a stream
+ * that is being captured into a graph (MX_ERR_CAPTURE).
  */
 int mx_linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, float* dX,
                        float* dW, int64_t T, int64_t in_features, int64_t out_features, int g,

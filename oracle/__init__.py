@@ -13,7 +13,7 @@ It is plain, slow and written to be checked against the paper by eye:
 * ``philox``   -- Philox4x32-10 (Salmon et al., SC'11), the counter-based generator
                   that supplies the sign vector and the dithering noise.
 * ``formats``  -- E2M1 element grid (Table 1; Sec. 2.5) and the E8M0 shared scale.
-* ``hadamard`` -- Sylvester Hadamard matrix (Eq. hadrec) and the blockwise random
+* ``hadamard`` -- Sylvester Hadamard matrix (the recursion of Sec. 3.2) and the blockwise random
                   Hadamard transform of Sec. 3.2.
 * ``mxquant``  -- Algorithm 2 (unbiased MXFP4 quantisation with stochastic
                   rounding, Eq. 1) and Algorithm 1 (nearest rounding).

@@ -3,12 +3,12 @@
 Test infrastructure only (see the package docstring).
 
 Sec. 3.2 defines the RHT as x <- H S x with S a random sign vector and H the
-Hadamard matrix given by the recursion Eq. (hadrec): H_n is built from four
+Hadamard matrix given by the recursion that Sec. 3.2 writes down: H_n is built from four
 copies of H_{n-1}, the lower-right one negated, starting from H_1 = [1].
 
 Readings:
 
-* Normalisation. Eq. (hadrec) puts a factor 2^{-n/2} into a recursion whose
+* Normalisation. The Hadamard recursion of Sec. 3.2 puts a factor 2^{-n/2} into a recursion whose
   H_{n-1} is already normalised, which cannot be what is meant; the intent is
   an orthogonal H (the paper notes H and diag(S) are orthogonal). The data
   path uses the +-1 Sylvester matrix, for which H H^T = g I, and the factor
@@ -29,7 +29,7 @@ import numpy as np
 
 
 def sylvester(g):
-    """The g x g +-1 Sylvester Hadamard matrix (Eq. hadrec without its scale factor), int64."""
+    """The g x g +-1 Sylvester Hadamard matrix (the Hadamard recursion of Sec. 3.2 without its scale factor), int64."""
     if g < 1 or (g & (g - 1)):
         raise ValueError("g must be a power of two")
     h = np.ones((1, 1), dtype=np.int64)
@@ -39,7 +39,7 @@ def sylvester(g):
 
 
 def hadamard_fp32(x):
-    """H_n x along the last axis of a float32 array, by the recursion of Eq. (hadrec).
+    """H_n x along the last axis of a float32 array, by the Hadamard recursion of Sec. 3.2.
 
     The length n of the last axis must be a power of two. Every add and subtract
     is a float32 operation, so each output is the FP32 value the recursion gives.

@@ -15,6 +15,7 @@ _LIB = None
 _STATUS = {
     0: "MX_OK", -1: "MX_ERR_NULL", -2: "MX_ERR_G", -3: "MX_ERR_SHAPE", -4: "MX_ERR_ALIGN",
     -5: "MX_ERR_HIP", -6: "MX_ERR_NOMEM", -7: "MX_ERR_DEVICE", -8: "MX_ERR_MODE", -9: "MX_ERR_FLAGS",
+    -10: "MX_ERR_CAPTURE",
 }
 
 # Quantiser modes (include/mxfp4.h, enum mx_mode): the method and the ablation
@@ -84,14 +85,6 @@ def _check(status):
         raise MxError(status, lib.mx_status_string(status).decode())
 
 
-def _ptr(t):
-    if t is None:
-        return None
-    if not t.is_contiguous():
-        raise ValueError("tensors must be contiguous (row-major)")
-    return t.data_ptr() or None
-
-
 def _stream(stream):
     import torch
     if stream is None:
@@ -99,58 +92,130 @@ def _stream(stream):
     return getattr(stream, "cuda_stream", stream)
 
 
+# Argument checks. The library trusts the sizes it is given: an output tensor
+# smaller than the sizes say would be written past its end on the device. So
+# every wrapper checks each tensor's dtype, shape and layout against the sizes
+# it passes, and that all tensors live on the current GPU, before calling the
+# library; a mismatch raises ValueError and nothing is called.
+
+def _dtypes(kind):
+    import torch
+    return {
+        "bf16": (torch.bfloat16, torch.int16, torch.uint16),     # bf16 values or their bit patterns
+        "u8": (torch.uint8,),
+        "f32": (torch.float32,),
+    }[kind]
+
+
+def _arg(t, name, kind, shape):
+    """Checks one tensor argument; returns its device pointer (None for an empty tensor)."""
+    if t is None:
+        raise ValueError(f"{name}: a tensor is required")
+    if t.dtype not in _dtypes(kind):
+        raise ValueError(f"{name}: dtype {t.dtype} is not one of {_dtypes(kind)}")
+    if tuple(t.shape) != tuple(int(d) for d in shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)} != expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: tensors must be contiguous (row-major)")
+    return t
+
+
+def _ptrs(*tensors):
+    """Device pointers of checked tensors, after checking they are all on the current GPU."""
+    import torch
+    live = [t for t in tensors if t is not None]
+    for t in live:
+        if t.device.type != "cuda":
+            raise ValueError(f"tensor on {t.device}: the library takes tensors on the current GPU")
+    if live:
+        cur = torch.cuda.current_device()
+        for t in live:
+            if t.device.index != cur:
+                raise ValueError(f"tensor on {t.device}, but the current device is cuda:{cur}")
+    return [None if t is None else (t.data_ptr() or None) for t in tensors]
+
+
+def _two_d(t, name):
+    if t is None or t.dim() != 2:
+        raise ValueError(f"{name}: a 2-D tensor is required")
+    return t.shape
+
+
 def quantized_shapes(rows, cols):
     """(codes shape, scales shape) of an MXFP4 matrix with logical shape [rows, cols]."""
     return (rows, cols // 2), (rows, cols // 32)
 
 
+def _quant_args(x, codes, scales, transposed):
+    if transposed:
+        cols, rows = _two_d(x, "x_t")
+    else:
+        rows, cols = _two_d(x, "x")
+    cs, ss = quantized_shapes(rows, cols)
+    _arg(x, "x_t" if transposed else "x", "bf16", x.shape)
+    _arg(codes, "codes", "u8", cs)
+    _arg(scales, "scales", "u8", ss)
+    return rows, cols, _ptrs(x, codes, scales)
+
+
 def mx_rht_sr_quantize(x, codes, scales, g, seed, stream=None):
     """Quantise row-major bf16 x [rows, cols] (blocks along cols) into codes/scales (uint8)."""
-    rows, cols = x.shape
-    _check(load_library().mx_rht_sr_quantize(_ptr(x), _ptr(codes), _ptr(scales), rows, cols, g,
-                                             seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
+    rows, cols, p = _quant_args(x, codes, scales, False)
+    _check(load_library().mx_rht_sr_quantize(*p, rows, cols, g, seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
 
 
 def mx_rht_sr_quantize_t(x_t, codes, scales, g, seed, stream=None):
     """Quantise the transpose of bf16 x_t [cols, rows]: logical matrix [rows, cols]."""
-    cols, rows = x_t.shape
-    _check(load_library().mx_rht_sr_quantize_t(_ptr(x_t), _ptr(codes), _ptr(scales), rows, cols, g,
-                                               seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
+    rows, cols, p = _quant_args(x_t, codes, scales, True)
+    _check(load_library().mx_rht_sr_quantize_t(*p, rows, cols, g, seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
 
 
 def mx_quantize(x, codes, scales, g, seed, mode, transposed=False, stream=None):
     """Quantise in any mode (MX_MODE_*). transposed=False: x is the row-major [rows, cols]
     matrix; transposed=True: x is stored [cols, rows] and the logical matrix is its transpose."""
-    if transposed:
-        cols, rows = x.shape
-    else:
-        rows, cols = x.shape
-    _check(load_library().mx_quantize(_ptr(x), _ptr(codes), _ptr(scales), rows, cols, g,
-                                      seed & 0xFFFFFFFFFFFFFFFF, mode, 1 if transposed else 0, _stream(stream)))
+    rows, cols, p = _quant_args(x, codes, scales, bool(transposed))
+    _check(load_library().mx_quantize(*p, rows, cols, g, seed & 0xFFFFFFFFFFFFFFFF, mode, 1 if transposed else 0,
+                                      _stream(stream)))
 
 
 def mx_gemm_f4(a_codes, a_scales, b_codes, b_scales, c, stream=None):
     """C[M, N] (float32) = deq(A) @ deq(B)^T for MXFP4 operands A [M, K], B [N, K]."""
-    m, kh = a_codes.shape
-    n = b_codes.shape[0]
-    _check(load_library().mx_gemm_f4(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales),
-                                     _ptr(c), m, n, 2 * kh, _stream(stream)))
+    m, kh = _two_d(a_codes, "a_codes")
+    n = _two_d(b_codes, "b_codes")[0]
+    k = 2 * kh
+    _arg(a_codes, "a_codes", "u8", (m, kh))
+    _arg(a_scales, "a_scales", "u8", (m, k // 32))
+    _arg(b_codes, "b_codes", "u8", (n, kh))
+    _arg(b_scales, "b_scales", "u8", (n, k // 32))
+    _arg(c, "c", "f32", (m, n))
+    _check(load_library().mx_gemm_f4(*_ptrs(a_codes, a_scales, b_codes, b_scales, c), m, n, k, _stream(stream)))
+
+
+def _backward_args(dy, x, w, dx, dw, db=None, dx_kind="f32"):
+    t, out_f = _two_d(dy, "dy")
+    in_f = _two_d(x, "x")[1]
+    _arg(dy, "dy", "bf16", (t, out_f))
+    _arg(x, "x", "bf16", (t, in_f))
+    _arg(w, "w", "bf16", (out_f, in_f))
+    _arg(dx, "dx", dx_kind, (t, in_f))
+    _arg(dw, "dw", "f32", (out_f, in_f))
+    if db is not None:
+        _arg(db, "db", "f32", (out_f,))
+    return t, in_f, out_f
 
 
 def mx_linear_backward(dy, x, w, dx, dw, g, seed, stream=None):
     """Algorithm 3: dX = 16/(9g) Q(dY) Q(W^T)^T, dW = 16/(9g) Q(dY^T) Q(x^T)^T (float32 outputs)."""
-    t, out_f = dy.shape
-    in_f = x.shape[1]
-    _check(load_library().mx_linear_backward(_ptr(dy), _ptr(x), _ptr(w), _ptr(dx), _ptr(dw), t, in_f,
-                                             out_f, g, seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
+    t, in_f, out_f = _backward_args(dy, x, w, dx, dw)
+    _check(load_library().mx_linear_backward(*_ptrs(dy, x, w, dx, dw), t, in_f, out_f, g,
+                                             seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
 
 
 def mx_linear_backward_mode(dy, x, w, dx, dw, g, seed, mode, stream=None):
     """mx_linear_backward with the operands quantised in mode `mode` (MX_MODE_*)."""
-    t, out_f = dy.shape
-    in_f = x.shape[1]
-    _check(load_library().mx_linear_backward_mode(_ptr(dy), _ptr(x), _ptr(w), _ptr(dx), _ptr(dw), t, in_f,
-                                                  out_f, g, seed & 0xFFFFFFFFFFFFFFFF, mode, _stream(stream)))
+    t, in_f, out_f = _backward_args(dy, x, w, dx, dw)
+    _check(load_library().mx_linear_backward_mode(*_ptrs(dy, x, w, dx, dw), t, in_f, out_f, g,
+                                                  seed & 0xFFFFFFFFFFFFFFFF, mode, _stream(stream)))
 
 
 def mx_linear_backward_workspace_bytes(t, in_features, out_features):
@@ -161,11 +226,9 @@ def mx_linear_backward_ex(dy, x, w, dx, dw, db, g, seed, mode=MX_MODE_RHT_SR, fl
     """Backward of y = x W^T + b: dX and dW by Algorithm 3 (dx float32, or bf16 with
     MX_BWD_DX_BF16), db = column sums of dY (db=None: no bias); MX_BWD_ACCUMULATE adds
     dW and db to the tensors' contents."""
-    t, out_f = dy.shape
-    in_f = x.shape[1]
-    _check(load_library().mx_linear_backward_ex(_ptr(dy), _ptr(x), _ptr(w), _ptr(dx), _ptr(dw), _ptr(db), t,
-                                                in_f, out_f, g, seed & 0xFFFFFFFFFFFFFFFF, mode, flags,
-                                                _stream(stream)))
+    t, in_f, out_f = _backward_args(dy, x, w, dx, dw, db, "bf16" if flags & MX_BWD_DX_BF16 else "f32")
+    _check(load_library().mx_linear_backward_ex(*_ptrs(dy, x, w, dx, dw, db), t, in_f, out_f, g,
+                                                seed & 0xFFFFFFFFFFFFFFFF, mode, flags, _stream(stream)))
 
 
 def mx_linear_backward_ex_workspace_bytes(t, in_features, out_features, g, mode=MX_MODE_RHT_SR, with_db=True):

@@ -117,6 +117,19 @@ class WorkspaceLease {
   Workspace* ws_ = nullptr;
 };
 
+// Entry points that enqueue work refuse a stream that is being captured into
+// a graph: a call may allocate or free workspace in stream order, and a graph
+// would also keep the workspace address it saw, which a later call that grows
+// the workspace frees. (An implicit capture of the legacy default stream, when
+// another stream captures in global mode, counts as capturing.)
+int check_not_capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  const hipError_t e = hipStreamIsCapturing(s, &cs);
+  if (e == hipErrorStreamCaptureImplicit) return MX_ERR_CAPTURE;
+  if (e != hipSuccess) return MX_ERR_HIP;
+  return cs == hipStreamCaptureStatusNone ? MX_OK : MX_ERR_CAPTURE;
+}
+
 bool valid_g(int g) { return g == 32 || g == 64 || g == 128 || g == 256; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -204,6 +217,7 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
     return MX_ERR_ALIGN;
   int st = check_device();
   if (st != MX_OK) return st;
+  if ((st = check_not_capturing(s)) != MX_OK) return st;
   // 16/9 undoes the 3/4 pre-scale of both operands (stochastic rounding only);
   // 1/g undoes H H^T = g I of the +-1 Hadamard (RHT modes only).
   const float alpha = (mode_has_sr(mode) ? 16.0f / 9.0f : 1.0f) / (float)(mode_has_rht(mode) ? g : 1);
@@ -278,6 +292,7 @@ const char* mx_status_string(int status) {
     case MX_ERR_DEVICE: return "MX_ERR_DEVICE: current device is not gfx950";
     case MX_ERR_MODE: return "MX_ERR_MODE: mode is not one of MX_MODE_*";
     case MX_ERR_FLAGS: return "MX_ERR_FLAGS: flags holds bits that are not MX_BWD_*";
+    case MX_ERR_CAPTURE: return "MX_ERR_CAPTURE: the stream is being captured into a graph";
     default: return "MX_ERR_UNKNOWN";
   }
 }
@@ -287,6 +302,7 @@ int mx_quantize(const uint16_t* in, uint8_t* codes, uint8_t* scales, int64_t row
   int st = validate_quant(in, codes, scales, rows, cols, g, transposed != 0, mode);
   if (st != MX_OK || rows == 0 || cols == 0) return st;
   if ((st = check_device()) != MX_OK) return st;
+  if ((st = check_not_capturing((hipStream_t)stream)) != MX_OK) return st;
   const mx::QuantSpec spec{in, codes, scales, rows, cols, seed, transposed != 0, false};
   return mx::launch_quant(&spec, 1, g, static_cast<mx::QuantMode>(mode), (hipStream_t)stream) ? MX_ERR_HIP
                                                                                                  : MX_OK;
@@ -312,6 +328,7 @@ int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B
   int st = check_device();
   if (st != MX_OK) return st;
   hipStream_t s = (hipStream_t)stream;
+  if ((st = check_not_capturing(s)) != MX_OK) return st;
   mx::GemmArgs g{A_codes, A_scales, B_codes, B_scales, C, M, N, K, 1.0f, false};
   // On the LDS-ring kernels the operands are first copied into the K-tiled
   // layout those kernels load fastest (one stage of a run of rows is one

@@ -202,3 +202,60 @@ def test_linear_backward_ex_workspace_bytes():
         assert wx(t, fin, fout, 0, binding.MX_MODE_SR, 1) == base + up(t // 32 * fout * 4)
     assert wx(64, 64, 64, 48, binding.MX_MODE_RHT_SR, 1) == 0
     assert wx(64, 64, 64, 64, 7, 1) == 0
+
+
+# --- Python binding argument checks (no GPU: CPU tensors never reach the library) ---
+
+def _t(shape, dtype):
+    import torch
+    return torch.zeros(shape, dtype=dtype)
+
+
+def test_binding_rejects_mismatched_shapes_and_dtypes():
+    import torch
+    u8, f32, b16 = torch.uint8, torch.float32, torch.bfloat16
+    m, n, k = 8, 16, 64
+    ok = dict(a_codes=_t((m, k // 2), u8), a_scales=_t((m, k // 32), u8), b_codes=_t((n, k // 2), u8),
+              b_scales=_t((n, k // 32), u8), c=_t((m, n), f32))
+    bad = [("b_codes", _t((n, k // 2 + 1), u8)), ("a_scales", _t((m, k // 32 + 1), u8)),
+           ("b_scales", _t((n + 1, k // 32), u8)), ("c", _t((m, n - 1), f32)), ("c", _t((m, n), b16)),
+           ("a_codes", _t((m, k // 2), torch.int8))]
+    for name, t in bad:
+        args = dict(ok, **{name: t})
+        with pytest.raises(ValueError, match=name.split("_")[0]):
+            binding.mx_gemm_f4(**args)
+    t_, fin, fout = 64, 32, 64
+    dy, x, w = _t((t_, fout), b16), _t((t_, fin), b16), _t((fout, fin), b16)
+    dx, dw, db = _t((t_, fin), f32), _t((fout, fin), f32), _t((fout,), f32)
+    for args in ((dy, _t((t_ + 1, fin), b16), w, dx, dw), (dy, x, _t((fout, fin + 1), b16), dx, dw),
+                 (dy, x, w, _t((t_, fin + 1), f32), dw), (dy, x, w, dx, _t((fout, fin), torch.float64)),
+                 (dy, x, w, _t((t_, fin), b16), dw)):
+        with pytest.raises(ValueError):
+            binding.mx_linear_backward(*args, 64, 0)
+    with pytest.raises(ValueError, match="db"):
+        binding.mx_linear_backward_ex(dy, x, w, dx, dw, _t((fout + 1,), f32), 64, 0)
+    # bf16 dX with MX_BWD_DX_BF16: a float32 dX of the right shape is the wrong kind
+    with pytest.raises(ValueError, match="dx"):
+        binding.mx_linear_backward_ex(dy, x, w, dx, dw, db, 64, 0, binding.MX_MODE_RHT_SR, binding.MX_BWD_DX_BF16)
+    with pytest.raises(ValueError, match="codes"):
+        binding.mx_rht_sr_quantize(dy, _t((t_, fout // 2 - 1), u8), _t((t_, fout // 32), u8), 64, 0)
+    with pytest.raises(ValueError, match="scales"):
+        # stored [cols = 32, rows = 64]: logical [64, 32], so codes [64, 16] and scales [64, 1]
+        binding.mx_rht_sr_quantize_t(_t((32, 64), b16), _t((64, 16), u8), _t((64, 2), u8), 32, 0)
+    with pytest.raises(ValueError, match="contiguous"):
+        binding.mx_rht_sr_quantize(_t((fout, t_), b16).t(), _t((t_, fout // 2), u8), _t((t_, fout // 32), u8),
+                                   64, 0)
+
+
+def test_binding_rejects_host_tensors():
+    """Well-formed arguments that live in host memory are refused before the library is called."""
+    import torch
+    dy = _t((64, 64), torch.bfloat16)
+    with pytest.raises(ValueError, match="current GPU"):
+        binding.mx_rht_sr_quantize(dy, _t((64, 32), torch.uint8), _t((64, 2), torch.uint8), 64, 0)
+
+
+def test_capture_status_is_declared():
+    text = open(HEADER).read()
+    assert re.search(r"MX_ERR_CAPTURE\s*=\s*-10", text)
+    assert binding._STATUS[-10] == "MX_ERR_CAPTURE"

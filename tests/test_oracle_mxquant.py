@@ -158,11 +158,14 @@ def test_sr_is_exact_mean_when_dither_resolution_divides():
 
 
 @pytest.mark.slow
-def test_quantiser_is_unbiased_for_three_quarters_of_rht_input():
+@pytest.mark.parametrize("g", [64, 128])
+def test_quantiser_is_unbiased_for_three_quarters_of_rht_input(g):
     """Lemma 3.1: E[deq(Q(x))] = (3/4) H S x. Empirical mean over 10^4 seeds
     (same sign vector, independent noise) within 3 sigma per element, sigma from
-    the closed-form variance, plus the 16-bit dither-resolution bias."""
-    g = 64
+    the closed-form variance, plus the 16-bit dither-resolution bias. g = 128 is
+    a case where the +-1 Hadamard differs from the orthonormal one by the
+    irrational factor sqrt(128): the estimator is unbiased for H S x all the
+    same."""
     bits = matrix((2, 128), seed=11, outlier_p=0.25, outlier_factor=50.0)
     hi = 0x5EED0000_00000000
     y = rht_fp32(bf16_bits_to_fp32(bits), sign_vector(hi, g))
