@@ -48,6 +48,9 @@ int launch_quant(const QuantSpec* specs, int count, int g, QuantMode mode, hipSt
 int colsum_reduce(const float* partial, float* out, int64_t rows, int64_t nblk, bool accumulate,
                   hipStream_t stream);
 
+// Sets `bytes` bytes (a multiple of 2, 2-byte aligned) at p to zero.
+int zero_fill(void* p, int64_t bytes, hipStream_t stream);
+
 // How a GEMM writes C: FP32 (overwrite), bf16 (round to nearest even of the
 // FP32 result, overwrite), or FP32 added to what C holds.
 enum class Store : int { kF32 = 0, kBf16 = 1, kAccF32 = 2 };
@@ -90,6 +93,18 @@ int launch_gemm(const GemmArgs* probs, int count, float* partial_ws, hipStream_t
 // to hipExtLaunchKernel, which records them at the kernel's start and end
 // (null events, and a plain launch, while tracing is off).
 bool profiling();
+// While a NoTraceScope lives, launches from this thread are not traced (used
+// for work enqueued on a stream that is being captured into a graph).
+class NoTraceScope {
+ public:
+  explicit NoTraceScope(bool active);
+  ~NoTraceScope();
+  NoTraceScope(const NoTraceScope&) = delete;
+  NoTraceScope& operator=(const NoTraceScope&) = delete;
+
+ private:
+  bool active_;
+};
 class TraceScope {
  public:
   TraceScope(const char* name, double work, bool flops);

@@ -36,9 +36,18 @@ hipEvent_t take_event() {
   return e;
 }
 
+thread_local int g_no_trace = 0;
+
 }  // namespace
 
-bool profiling() { return g_on.load(std::memory_order_acquire); }
+bool profiling() { return g_no_trace == 0 && g_on.load(std::memory_order_acquire); }
+
+NoTraceScope::NoTraceScope(bool active) : active_(active) {
+  if (active_) ++g_no_trace;
+}
+NoTraceScope::~NoTraceScope() {
+  if (active_) --g_no_trace;
+}
 
 TraceScope::TraceScope(const char* name, double work, bool flops) {
   if (!profiling()) return;

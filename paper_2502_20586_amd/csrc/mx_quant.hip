@@ -807,7 +807,25 @@ __global__ __launch_bounds__(64 * kColsumWaves) void colsum_reduce_kernel(const 
   }
 }
 
+// Clears n 16-bit words: every output the library clears is made of bf16 or
+// FP32 elements, so a 2-byte granularity covers all of them. A kernel rather
+// than a memset node keeps the clear well-defined inside a captured graph.
+__global__ __launch_bounds__(256) void zero_fill_kernel(uint16_t* p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
+}
+
 }  // namespace
+
+int zero_fill(void* p, int64_t bytes, hipStream_t stream) {
+  if (bytes <= 0) return 0;
+  const int64_t n = bytes / 2;
+  const int64_t wgs = (n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096;
+  TraceScope trace("zero_fill", (double)bytes, false);
+  hipExtLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)wgs), dim3(256), 0, stream, trace.start(), trace.stop(), 0,
+                        static_cast<uint16_t*>(p), n);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
 
 int colsum_reduce(const float* partial, float* out, int64_t rows, int64_t nblk, bool accumulate,
                   hipStream_t stream) {
