@@ -42,10 +42,18 @@ def lib_path():
 
 
 def load_library():
-    """Load libmxfp4.so from the package directory (built by build.py). Raises if absent."""
+    """Load libmxfp4.so from the package directory (built by build.py). Raises if absent.
+
+    torch is imported first: the library then binds to the HIP runtime that
+    torch has loaded (it needs libamdhip64.so.7, which torch's copy provides
+    under that name). Loaded the other way round, the library would pull in
+    the system's HIP runtime and torch its own, and two runtimes in one
+    process do not share devices or streams (the library's calls then fail
+    with MX_ERR_HIP)."""
     global _LIB
     if _LIB is not None:
         return _LIB
+    import torch  # noqa: F401  (see above)
     path = lib_path()
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2502_20586_amd.build`")

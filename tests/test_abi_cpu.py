@@ -259,3 +259,20 @@ def test_capture_status_is_declared():
     text = open(HEADER).read()
     assert re.search(r"MX_ERR_CAPTURE\s*=\s*-10", text)
     assert binding._STATUS[-10] == "MX_ERR_CAPTURE"
+
+
+def test_binding_loads_one_hip_runtime():
+    """load_library() in a fresh process, before anything imports torch: the
+    library must bind to the HIP runtime torch loads, so the process maps one
+    libamdhip64 (two runtimes do not share devices or streams)."""
+    import subprocess
+    import sys
+    _lib()
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "import paper_2502_20586_amd.binding as b\n"
+            "b.load_library()\n"
+            "print(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    runtimes = eval(out.stdout.strip().splitlines()[-1])
+    assert len(runtimes) == 1, runtimes
