@@ -91,7 +91,8 @@ enum mx_status {
   MX_ERR_DEVICE = -7,  /* the current device is not a gfx950 GPU */
   MX_ERR_MODE = -8,    /* mode is not one of MX_MODE_* */
   MX_ERR_FLAGS = -9,   /* flags holds a bit that is not one of MX_BWD_* */
-  MX_ERR_CAPTURE = -10 /* the stream is being captured into a graph */
+  MX_ERR_CAPTURE = -10, /* the stream is being captured into a graph */
+  MX_ERR_TOO_LARGE = -11 /* more scratch than mx_linear_backward_noalloc holds */
 };
 
 /*
@@ -206,6 +207,30 @@ int mx_linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
 int mx_linear_backward_mode(const uint16_t* dY, const uint16_t* X, const uint16_t* W, float* dX, float* dW,
                             int64_t T, int64_t in_features, int64_t out_features, int g, uint64_t seed,
                             int mode, void* stream);
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * result as mx_linear_backward, bit for bit, with no allocation at all.
+ *   Arguments, layouts and alignment as for mx_linear_backward; the caller
+ *   still provides dY, X, W, dX and dW.
+ *   Scratch (the quantised operands and any split-K partial sums, the bytes
+ *   mx_linear_backward_workspace_bytes reports) comes from a fixed array of
+ *   MX_NOALLOC_SCRATCH_BYTES (64 MiB) in device memory that the library holds
+ *   on every GPU it runs this call on, from the first such call until the
+ *   process ends. A problem that needs more returns MX_ERR_TOO_LARGE and
+ *   enqueues nothing: 64 MiB holds any linear of a GPT-345M-shaped block
+ *   (4096 tokens, hidden 1024), not GPT-1.3B's MLP linears.
+ *   All calls on one GPU share that array: calls that overlap in time on one
+ *   GPU (other streams, other threads) race and give wrong results; calls
+ *   ordered on one stream are safe. Nothing in it needs to start at zero.
+ *   This call calls no hipMalloc/hipFree or allocating routine, and does not
+ *   refuse a stream that is being captured (its launches are then not traced).
+ */
+#define MX_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int mx_linear_backward_noalloc(const uint16_t* dY, const uint16_t* X, const uint16_t* W, float* dX,
+                               float* dW, int64_t T, int64_t in_features, int64_t out_features, int g,
+                               uint64_t seed, void* stream);
 
 /* Bytes of stream-ordered scratch mx_linear_backward allocates for a shape. */
 int64_t mx_linear_backward_workspace_bytes(int64_t T, int64_t in_features, int64_t out_features);

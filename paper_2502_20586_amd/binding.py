@@ -15,8 +15,11 @@ _LIB = None
 _STATUS = {
     0: "MX_OK", -1: "MX_ERR_NULL", -2: "MX_ERR_G", -3: "MX_ERR_SHAPE", -4: "MX_ERR_ALIGN",
     -5: "MX_ERR_HIP", -6: "MX_ERR_NOMEM", -7: "MX_ERR_DEVICE", -8: "MX_ERR_MODE", -9: "MX_ERR_FLAGS",
-    -10: "MX_ERR_CAPTURE",
+    -10: "MX_ERR_CAPTURE", -11: "MX_ERR_TOO_LARGE",
 }
+
+# Scratch held by mx_linear_backward_noalloc on each GPU (include/mxfp4.h).
+MX_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 # Quantiser modes (include/mxfp4.h, enum mx_mode): the method and the ablation
 # rows of Table 2.
@@ -73,6 +76,8 @@ def load_library():
     lib.mx_gemm_f4.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
     lib.mx_linear_backward.restype = ci
     lib.mx_linear_backward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ci, u64, vp]
+    lib.mx_linear_backward_noalloc.restype = ci
+    lib.mx_linear_backward_noalloc.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ci, u64, vp]
     lib.mx_linear_backward_workspace_bytes.restype = i64
     lib.mx_linear_backward_workspace_bytes.argtypes = [i64, i64, i64]
     lib.mx_linear_backward_ex.restype = ci
@@ -217,6 +222,14 @@ def mx_linear_backward(dy, x, w, dx, dw, g, seed, stream=None):
     t, in_f, out_f = _backward_args(dy, x, w, dx, dw)
     _check(load_library().mx_linear_backward(*_ptrs(dy, x, w, dx, dw), t, in_f, out_f, g,
                                              seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
+
+
+def mx_linear_backward_noalloc(dy, x, w, dx, dw, g, seed, stream=None):
+    """mx_linear_backward with its scratch in the library's fixed per-GPU array (no allocation;
+    problems needing more than MX_NOALLOC_SCRATCH_BYTES raise MX_ERR_TOO_LARGE)."""
+    t, in_f, out_f = _backward_args(dy, x, w, dx, dw)
+    _check(load_library().mx_linear_backward_noalloc(*_ptrs(dy, x, w, dx, dw), t, in_f, out_f, g,
+                                                     seed & 0xFFFFFFFFFFFFFFFF, _stream(stream)))
 
 
 def mx_linear_backward_mode(dy, x, w, dx, dw, g, seed, mode, stream=None):

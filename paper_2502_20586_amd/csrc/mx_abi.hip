@@ -130,6 +130,35 @@ int check_not_capturing(hipStream_t s) {
   return cs == hipStreamCaptureStatusNone ? MX_OK : MX_ERR_CAPTURE;
 }
 
+// Scratch of mx_linear_backward_noalloc: a fixed array in device memory, one
+// copy per GPU that the library runs on, held until the process ends. In host
+// code `scratch` only names the variable; its device address on a GPU is what
+// hipGetSymbolAddress returns with that GPU current, looked up once per device
+// and kept. Every call on a GPU shares that GPU's copy and leaves in it what
+// it wrote (the quantised operands and split-K partial sums, all of which the
+// next call writes before it reads them, so nothing has to start at zero);
+// calls that overlap on one GPU race.
+constexpr int64_t kNoallocScratchBytes = MX_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];
+
+int scratch_for_device(void** out) {
+  *out = nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MX_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MX_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MX_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MX_OK;
+}
+
 bool valid_g(int g) { return g == 32 || g == 64 || g == 128 || g == 256; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -192,9 +221,12 @@ constexpr unsigned kKnownFlags = MX_BWD_DX_BF16 | MX_BWD_ACCUMULATE;
 
 // Algorithm 3 with the options of mx_linear_backward_ex (the contract is in
 // include/mxfp4.h).
+// noalloc: scratch comes from the fixed per-GPU array instead of the
+// stream's workspace, nothing is allocated, and a capturing stream is allowed
+// (its launches are then not traced).
 int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, void* dX, float* dW, float* db,
                     int64_t T, int64_t in_features, int64_t out_features, int g, uint64_t seed, int mode,
-                    unsigned flags, hipStream_t s) {
+                    unsigned flags, hipStream_t s, bool noalloc = false) {
   if (!valid_mode(mode)) return MX_ERR_MODE;
   if (flags & ~kKnownFlags) return MX_ERR_FLAGS;
   if (mode_has_rht(mode) && !valid_g(g)) return MX_ERR_G;
@@ -217,7 +249,12 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
     return MX_ERR_ALIGN;
   int st = check_device();
   if (st != MX_OK) return st;
-  if ((st = check_not_capturing(s)) != MX_OK) return st;
+  bool capturing = false;
+  if ((st = check_not_capturing(s)) == MX_ERR_CAPTURE && noalloc)
+    capturing = true;
+  else if (st != MX_OK)
+    return st;
+  const mx::NoTraceScope no_trace(capturing);
   // 16/9 undoes the 3/4 pre-scale of both operands (stochastic rounding only);
   // 1/g undoes H H^T = g I of the +-1 Hadamard (RHT modes only).
   const float alpha = (mode_has_sr(mode) ? 16.0f / 9.0f : 1.0f) / (float)(mode_has_rht(mode) ? g : 1);
@@ -225,13 +262,9 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
   // K = 0 for a GEMM (T == 0 or out == 0): its product is all zeros, so an
   // overwritten output is cleared and an accumulated one is left as it is.
   if (T == 0 || out_features == 0) {
-    if (need_dx && hipMemsetAsync(dX, 0, (size_t)(T * in_features) * (dx_bf16 ? 2 : 4), s) != hipSuccess)
-      return MX_ERR_HIP;
-    if (need_dw && !accumulate &&
-        hipMemsetAsync(dW, 0, (size_t)(out_features * in_features) * 4, s) != hipSuccess)
-      return MX_ERR_HIP;
-    if (need_db && !accumulate && hipMemsetAsync(db, 0, (size_t)out_features * 4, s) != hipSuccess)
-      return MX_ERR_HIP;
+    if (need_dx && mx::zero_fill(dX, T * in_features * (dx_bf16 ? 2 : 4), s)) return MX_ERR_HIP;
+    if (need_dw && !accumulate && mx::zero_fill(dW, out_features * in_features * 4, s)) return MX_ERR_HIP;
+    if (need_db && !accumulate && mx::zero_fill(db, out_features * 4, s)) return MX_ERR_HIP;
     return MX_OK;
   }
 
@@ -243,7 +276,12 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
   const int64_t bytes = layout_workspace(T, in_features, out_features, nullptr, nullptr, nullptr, colsum_bytes);
   void* ws = nullptr;
   WorkspaceLease lease;
-  if ((st = lease.acquire(bytes, s, &ws)) != MX_OK) return st;
+  if (noalloc) {
+    if (bytes > kNoallocScratchBytes) return MX_ERR_TOO_LARGE;
+    if ((st = scratch_for_device(&ws)) != MX_OK) return st;
+  } else if ((st = lease.acquire(bytes, s, &ws)) != MX_OK) {
+    return st;
+  }
   layout_workspace(T, in_features, out_features, static_cast<uint8_t*>(ws), q, &partial, colsum_bytes, &colsum);
 
   int fail = 0;
@@ -293,6 +331,8 @@ const char* mx_status_string(int status) {
     case MX_ERR_MODE: return "MX_ERR_MODE: mode is not one of MX_MODE_*";
     case MX_ERR_FLAGS: return "MX_ERR_FLAGS: flags holds bits that are not MX_BWD_*";
     case MX_ERR_CAPTURE: return "MX_ERR_CAPTURE: the stream is being captured into a graph";
+    case MX_ERR_TOO_LARGE:
+      return "MX_ERR_TOO_LARGE: the problem needs more scratch than mx_linear_backward_noalloc holds";
     default: return "MX_ERR_UNKNOWN";
   }
 }
@@ -395,6 +435,13 @@ int mx_linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                        void* stream) {
   return mx_linear_backward_mode(dY, X, W, dX, dW, T, in_features, out_features, g, seed, MX_MODE_RHT_SR,
                                  stream);
+}
+
+int mx_linear_backward_noalloc(const uint16_t* dY, const uint16_t* X, const uint16_t* W, float* dX, float* dW,
+                               int64_t T, int64_t in_features, int64_t out_features, int g, uint64_t seed,
+                               void* stream) {
+  return linear_backward(dY, X, W, dX, dW, nullptr, T, in_features, out_features, g, seed, MX_MODE_RHT_SR, 0u,
+                         (hipStream_t)stream, true);
 }
 
 }  // extern "C"
