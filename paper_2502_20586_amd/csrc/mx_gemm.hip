@@ -471,7 +471,8 @@ __global__ __launch_bounds__(kThreads) void gemm_f4_kernel(Group grp) {
 //   slot is free again one stage early: three stages of loads are in flight
 //   beyond the one being read. (With one 64-K step of read-ahead the fragment
 //   reads, slowed by the direct-to-LDS writes competing for LDS, stalled the
-//   MFMAs.)
+//   MFMAs.) At 256 x 256 the loads and reads are spread among the MFMAs in a
+//   fixed order (see the stage functions).
 // * Each operand is read through a buffer resource that starts at the tile's
 //   first row and ends with the operand: rows past M (N) fall outside it and
 //   load as zeros, and code 0 contributes 0 whatever its scale, so ragged M and
@@ -627,27 +628,35 @@ __global__ __launch_bounds__(kThreads, ring::Cfg<BT>::kWgPerCu) void gemm_ring_k
     s_dst[k] = (uint32_t)(2 * C::kCode + (is_a ? 0 : C::kScale) + c * 256);
   }
 
-  // Loads of stage s (of the K window) into slot s % 4. A stage past the end
-  // of the window goes through a null resource: every load returns zeros
-  // without touching memory, into a slot nobody reads again.
+  // Loads of stage s (of the K window) into slot s % 4: load q of the stage's
+  // kLoads is A's code load q, B's code load q - kCodeLoads, or a scale load.
+  // A stage past the end of the window goes through a null resource: every
+  // load returns zeros without touching memory, into a slot nobody reads again.
   const int ksteps_all = (int)(pos.K / ring::kBK);
   const v4i rnull = buffer_rsrc(nullptr, 0);
-  auto issue = [&](int s) {
+  struct LoadRes {
+    v4i a, b, sa, sb;
+  };
+  auto load_res = [&](int s) {
     const bool live = s < ksteps_all;
+    return LoadRes{live ? rsa : rnull, live ? rsb : rnull, live ? rssa : rnull, live ? rssb : rnull};
+  };
+  auto issue_one = [&](int s, const LoadRes& r, int q) {
     const uint32_t slot = lds0 + (uint32_t)((s & 3) * C::kSlot);
-    const v4i ra = live ? rsa : rnull, rb = live ? rsb : rnull;
-    const v4i rsc_a = live ? rssa : rnull, rsc_b = live ? rssb : rnull;
-    const uint32_t ka = (uint32_t)s * a_csp, kb = (uint32_t)s * b_csp;
+    if (q < C::kCodeLoads) {
+      lds_load_b128(r.a, a_off[q] + (uint32_t)s * a_csp, slot + wave * (BT / 4) * kRow + q * 1024);
+    } else if (q < 2 * C::kCodeLoads) {
+      const int j = q - C::kCodeLoads;
+      lds_load_b128(r.b, b_off[j] + (uint32_t)s * b_csp, slot + C::kCode + wave * (BT / 4) * kRow + j * 1024);
+    } else {
+      const int k = q - 2 * C::kCodeLoads;
+      lds_load_b32(s_is_a[k] ? r.sa : r.sb, s_off[k] + (uint32_t)s * (s_is_a[k] ? a_ssp : b_ssp), slot + s_dst[k]);
+    }
+  };
+  auto issue = [&](int s) {
+    const LoadRes r = load_res(s);
 #pragma unroll
-    for (int j = 0; j < C::kCodeLoads; ++j)
-      lds_load_b128(ra, a_off[j] + ka, slot + wave * (BT / 4) * kRow + j * 1024);
-#pragma unroll
-    for (int j = 0; j < C::kCodeLoads; ++j)
-      lds_load_b128(rb, b_off[j] + kb, slot + C::kCode + wave * (BT / 4) * kRow + j * 1024);
-#pragma unroll
-    for (int k = 0; k < C::kScaleLoads; ++k)
-      lds_load_b32(s_is_a[k] ? rsc_a : rsc_b, s_off[k] + (uint32_t)s * (s_is_a[k] ? a_ssp : b_ssp),
-                   slot + s_dst[k]);
+    for (int q = 0; q < C::kLoads; ++q) issue_one(s, r, q);
   };
 
   // Reads of this lane: fragment rows wm WT + 32 i + lrow (A), wn WT + 32 j + lrow (B).
@@ -702,12 +711,56 @@ __global__ __launch_bounds__(kThreads, ring::Cfg<BT>::kWgPerCu) void gemm_ring_k
     };
     // One stage s: wait until this wave's reads of stage s (issued during the
     // previous stage) are done and stage s + 1 has landed, then a barrier, after
-    // which every wave has read slot s % 4 and stage s + 1 is visible; loads of
-    // stage s + 4 into slot s % 4; stage s + 1's reads interleaved with stage
-    // s's 32 MFMAs, which take their operands from registers. So a stage's
-    // reads have a whole stage of MFMAs to land, and its loads three stages.
-    // Stages past the end load zeros through the null resource.
-    auto stage = [&](int s, StageFrags& cur, StageFrags& nxt) {
+    // which every wave has read slot s % 4 and stage s + 1 is visible; then
+    // stage s's 2 TT^2 MFMAs from registers, with the reads of stage s + 1 and
+    // the loads of stage s + 4 (into slot s % 4) among them. So a stage's reads
+    // have a whole stage of MFMAs to land, and its loads three stages. Stages
+    // past the end load zeros through the null resource.
+    //
+    // 256 x 256 (one wave per SIMD): the order is fixed. One fragment read
+    // after every second MFMA (the two scale reads two thirds through), and the
+    // ten loads one after every third MFMA. Issued together at the top of the
+    // stage, the loads held up the MFMAs behind them: spread out, the GEMMs of
+    // the GPT-6.7B block ran 8% faster (828 -> 759 us per launch, same-box A/B).
+    // Moving the loads or the scale reads by a slot changed nothing measurable.
+    auto stage_fixed = [&](int s, StageFrags& cur, StageFrags& nxt) {
+      wait_and_sync<2 * C::kLoads>();
+      int sai[TT], sbj[TT];
+#pragma unroll
+      for (int i = 0; i < TT; ++i) sai[i] = (int)(cur.sa.w[i] >> sh);
+#pragma unroll
+      for (int j = 0; j < TT; ++j) sbj[j] = (int)(cur.sb.w[j] >> sh);
+      const uint8_t* slot = smem + ((s + 1) & 3) * C::kSlot;
+      const LoadRes lr = load_res(s + 4);
+      // read r of stage s + 1: a[0][*], b[0][*], a[1][*], b[1][*], then the scale words
+      auto read_one = [&](int r) {
+        if (r < TT) nxt.a[0][r] = *reinterpret_cast<const uint4*>(slot + a_rd + r * 32 * kRow + u0);
+        else if (r < 2 * TT) nxt.b[0][r - TT] = *reinterpret_cast<const uint4*>(slot + b_rd + (r - TT) * 32 * kRow + u0);
+        else if (r < 3 * TT) nxt.a[1][r - 2 * TT] = *reinterpret_cast<const uint4*>(slot + a_rd + (r - 2 * TT) * 32 * kRow + u1);
+        else if (r < 4 * TT) nxt.b[1][r - 3 * TT] = *reinterpret_cast<const uint4*>(slot + b_rd + (r - 3 * TT) * 32 * kRow + u1);
+        else if (r == 4 * TT) nxt.sa = read_scales<TT>(slot + sa_rd);
+        else nxt.sb = read_scales<TT>(slot + sb_rd);
+      };
+      constexpr int kMfma = 2 * TT * TT;
+#pragma unroll
+      for (int m = 0; m < kMfma; ++m) {
+        const int kk = m / (TT * TT), i = (m % (TT * TT)) / TT, j = m % TT;
+        acc[i][j] = kk == 0 ? __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_frag(cur.a[0][i]), as_frag(cur.b[0][j]),
+                                                                            acc[i][j], 4, 4, 0, sai[i], 0, sbj[j])
+                            : __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_frag(cur.a[1][i]), as_frag(cur.b[1][j]),
+                                                                            acc[i][j], 4, 4, 2, sai[i], 2, sbj[j]);
+        if (m % 3 == 1 && (m - 1) / 3 < C::kLoads) issue_one(s + 4, lr, (m - 1) / 3);
+        if (m % 2 == 0 && m / 2 < 4 * TT) read_one(m / 2);
+        if (m == kMfma / 2 + 1) read_one(4 * TT);
+        if (m == kMfma / 2 + 3) read_one(4 * TT + 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // 128 x 128 (two workgroups per CU, eight MFMAs per stage): the loads at the
+    // top and the compiler's own order for the rest, 3% and then 1.5-4.4%
+    // faster at GPT-345M than fixed orders; spreading the loads as above changed
+    // nothing there.
+    auto stage_free = [&](int s, StageFrags& cur, StageFrags& nxt) {
       wait_and_sync<2 * C::kLoads>();
       issue(s + 4);
       int sai[TT], sbj[TT];
@@ -721,20 +774,6 @@ __global__ __launch_bounds__(kThreads, ring::Cfg<BT>::kWgPerCu) void gemm_ring_k
 #pragma unroll
       for (int j = 0; j < TT; ++j) nxt.b[0][j] = *reinterpret_cast<const uint4*>(slot + b_rd + j * 32 * kRow + u0);
       mfma_step(cur, 0, sai, sbj);
-      // 256 x 256: one fragment read between every TT / 2 MFMAs, so no burst of
-      // reads holds up the MFMA issue. 128 x 128 (four MFMAs and four reads
-      // per 64-K step, two workgroups per CU) runs 3% faster on the GPT-345M
-      // shapes with the compiler's own order.
-      if constexpr (TT == 4) {
-#pragma unroll
-        for (int g = 0; g < 2 * TT; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // LDS read
-          __builtin_amdgcn_sched_group_barrier(0x008, TT / 2, 0);  // MFMA
-        }
-      }
-      // (At 128 x 128 the whole stage is left to the compiler: GEMM time 1.5-4%
-      // lower than with this barrier between its two 64-K steps.)
-      if constexpr (TT == 4) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TT; ++i) nxt.a[1][i] = *reinterpret_cast<const uint4*>(slot + a_rd + i * 32 * kRow + u1);
 #pragma unroll
@@ -742,15 +781,13 @@ __global__ __launch_bounds__(kThreads, ring::Cfg<BT>::kWgPerCu) void gemm_ring_k
       nxt.sa = read_scales<TT>(slot + sa_rd);
       nxt.sb = read_scales<TT>(slot + sb_rd);
       mfma_step(cur, 1, sai, sbj);
-      if constexpr (TT == 4) {
-#pragma unroll
-        for (int g = 0; g < 2 * TT; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, TT / 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);         // the scale words
-      }
       __builtin_amdgcn_sched_barrier(0);
+    };
+    auto stage = [&](int s, StageFrags& cur, StageFrags& nxt) {
+      if constexpr (TT == 4)
+        stage_fixed(s, cur, nxt);
+      else
+        stage_free(s, cur, nxt);
     };
     issue(0);
     issue(1);
