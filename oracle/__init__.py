@@ -21,6 +21,9 @@ It is plain, slow and written to be checked against the paper by eye:
                   (Appendix C, proof of Lemma 3.1).
 * ``backward`` -- Algorithm 3, the linear-layer backward pass; the bias gradient
                   1^T dY (Sec. 2.2) and accumulation into main gradients.
+* ``variance`` -- the variance of Algorithm 3's inner-product estimator and the
+                  flush-to-zero probability, in closed form from the rounding
+                  rule (the variance theorem of Sec. 3.2 and its figure; Sec. 4.1).
 
 Every reading taken where the paper is silent or garbled is listed in the
 docstring of the function that takes it.
@@ -33,6 +36,7 @@ from .mxquant import (shared_exponent_byte, mx_normalize, sr_e2m1, quantize_rht_
                       quantize_nr, pack_codes, unpack_codes)
 from .gemm import dequantize, gemm_f64
 from .backward import linear_backward, bias_grad, linear_backward_accumulate
+from .variance import sr_moments, estimator_alpha, inner_product_variance, expected_zero_codes
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_scalar", "sign_vector", "noise16",
@@ -41,4 +45,5 @@ __all__ = [
     "shared_exponent_byte", "mx_normalize", "sr_e2m1", "quantize_rht_sr", "quantize_nr",
     "pack_codes", "unpack_codes",
     "dequantize", "gemm_f64", "linear_backward", "bias_grad", "linear_backward_accumulate",
+    "sr_moments", "estimator_alpha", "inner_product_variance", "expected_zero_codes",
 ]

@@ -133,6 +133,24 @@ QUANT_SWEEP = dict(shapes=[(4096, 4096), (8192, 8192), (16384, 16384), (32768, 1
 RHT_OVERHEAD = dict(shapes=[(32768, 8192, 8192), (16384, 28672, 28672)], g=64, data_seed=6)
 
 
+# Sample vectors of the variance study (the figure of Sec. 3.2): A, B in R^b,
+# A = z + m o with z ~ N(0, I), m ~ Bernoulli(p) per element and o ~ N(0, 5 I)
+# (read as variance 5); n samples as the rows of an [n, b] matrix.
+FIG2 = dict(n=4096, b=[32, 64, 128, 256, 512, 1024, 2048, 4096], p=[0.0, 0.01, 0.05], outlier_var=5.0,
+            data_seed=7)
+
+
+def mixture_vectors(n, b, p, seed, outlier_var=5.0):
+    """[n, b] bf16 bit patterns: N(0, 1) entries plus, with probability p per
+    entry, an independent N(0, outlier_var) term; float64 draws rounded to
+    float32, then to bf16."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    z = rng.standard_normal((n, b))
+    m = rng.random((n, b)) < p
+    o = rng.standard_normal((n, b)) * np.sqrt(outlier_var)
+    return fp32_to_bf16_bits((z + np.where(m, o, 0.0)).astype(np.float32))
+
+
 def linear_inputs(config, linear):
     """(dY [T, out], x [T, in], W [out, in]) bf16 bit patterns for one linear of a config."""
     cfg = CONFIGS[config]
