@@ -119,6 +119,9 @@ def parse():
                          "--calib-copy, then exit")
     ap.add_argument("--rht-overhead", action="store_true",
                     help="RHT overhead study: GEMMs at the paper's 7B / 70B shapes in every quantiser mode")
+    ap.add_argument("--rht-variance", action="store_true",
+                    help="variance of the SR inner-product estimator with and without the RHT (the figure of "
+                         "Sec. 3.2) and the flush-to-zero statistic, through the HIP path")
     ap.add_argument("--configs", action="store_true",
                     help="instead of the step: GPT-1.3B (every g) and GPT-6.7B block backward end to end, "
                          "with BF16 / FP8 GEMM baselines on the same shapes")
@@ -320,6 +323,94 @@ def rht_overhead(torch, mx, reps=10):
         del a, b, ac, asc, bc, bsc
         torch.cuda.empty_cache()
     return res
+
+
+def rht_variance(torch, mx, draws=64, oracle_rows=256):
+    """The variance study of Sec. 3.2 (its figure) through the HIP path, and
+    the flush-to-zero statistic of Sec. 4.1.
+
+    Variance: for every sample length b and outlier rate p, n = 4096 sample
+    pairs A_i, B_i (rows of [n, b] matrices, workloads.mixture_vectors) are
+    quantised by mx_quantize with `draws` independent noise draws (one sign
+    vector), without the RHT (SR) and with it (RHT + SR, g = b up to 256, the
+    blockwise g = 256 beyond), and multiplied by mx_gemm_f4; the diagonal of
+    alpha C is the estimate alpha Q(A_i)^T Q(B_i) of A_i^T B_i. Reported: its
+    sample variance over the draws, averaged over the rows, per mode, and the
+    ratio SR / RHT + SR; beside it the oracle's exact variance (closed form
+    from the rounding rule) averaged over the first `oracle_rows` rows, with
+    the GPU's average over the same rows. Also the fraction of zero codes.
+
+    Flush to zero: the GPT-6.7B QKV output gradient dY (heavy-tailed, with
+    x1000 block outliers) quantised in each mode; fraction of its nonzero
+    elements whose code is 0 (with the RHT: of all elements, the transformed
+    values being nonzero)."""
+    import oracle
+    import workloads
+    cfg = workloads.FIG2
+    n = cfg["n"]
+    rows = []
+    modes = (("sr", mx.MX_MODE_SR, False), ("rht_sr", mx.MX_MODE_RHT_SR, True))
+    for b in cfg["b"]:
+        g = min(b, 256)
+        for p in cfg["p"]:
+            a_bits = workloads.mixture_vectors(n, b, p, [cfg["data_seed"], b, int(p * 1000), 0], cfg["outlier_var"])
+            b_bits = workloads.mixture_vectors(n, b, p, [cfg["data_seed"], b, int(p * 1000), 1], cfg["outlier_var"])
+            da = torch.from_numpy(a_bits.view(np.int16)).cuda()
+            db = torch.from_numpy(b_bits.view(np.int16)).cuda()
+            ac = torch.empty((n, b // 2), dtype=torch.uint8, device="cuda")
+            asc = torch.empty((n, b // 32), dtype=torch.uint8, device="cuda")
+            bc, bsc = torch.empty_like(ac), torch.empty_like(asc)
+            c = torch.empty((n, n), dtype=torch.float32, device="cuda")
+            hi = 0x0F26_0000_0000_0000 | (b << 32)
+            row = {"b": b, "p": p, "g": g, "n": n, "draws": draws}
+            for name, mode, rht in modes:
+                est = torch.empty((draws, n), dtype=torch.float64, device="cuda")
+                zeros = torch.zeros((), dtype=torch.float64, device="cuda")
+                for d in range(draws):
+                    mx.mx_quantize(da, ac, asc, g, hi | (2 * d), mode)
+                    mx.mx_quantize(db, bc, bsc, g, hi | (2 * d + 1), mode)
+                    mx.mx_gemm_f4(ac, asc, bc, bsc, c)
+                    est[d] = torch.diagonal(c).double()
+                    zeros += (((ac & 7) == 0).sum() + (((ac >> 4) & 7) == 0).sum()).double()
+                est *= oracle.estimator_alpha(g, rht)
+                var = est.var(dim=0).cpu().numpy()
+                exact = oracle.inner_product_variance(a_bits[:oracle_rows], b_bits[:oracle_rows], g, hi, hi | 1, rht)
+                row[name] = {"mean_var": float(var.mean()), "mean_var_first_rows": float(var[:oracle_rows].mean()),
+                             "oracle_mean_var_first_rows": float(exact.mean()),
+                             "zero_code_frac": float(zeros.item()) / (draws * n * b)}
+            row["ratio_sr_over_rht"] = row["sr"]["mean_var"] / row["rht_sr"]["mean_var"]
+            rows.append(row)
+            print(f"[var] b={b} p={p}: SR {row['sr']['mean_var']:.4g} (oracle {row['sr']['oracle_mean_var_first_rows']:.4g}"
+                  f" vs {row['sr']['mean_var_first_rows']:.4g}), RHT+SR {row['rht_sr']['mean_var']:.4g} (oracle "
+                  f"{row['rht_sr']['oracle_mean_var_first_rows']:.4g} vs {row['rht_sr']['mean_var_first_rows']:.4g}), "
+                  f"ratio {row['ratio_sr_over_rht']:.2f}", file=sys.stderr, flush=True)
+            del da, db, ac, asc, bc, bsc, c
+    # flush to zero on a GPT-6.7B output gradient
+    dy, _, _ = workloads.linear_inputs("gpt6.7b", "qkv")
+    t, fout = dy.shape
+    ddy = torch.from_numpy(dy.view(np.int16)).cuda()
+    nz = int(np.count_nonzero(dy & 0x7FFF))
+    codes = torch.empty((t, fout // 2), dtype=torch.uint8, device="cuda")
+    scales = torch.empty((t, fout // 32), dtype=torch.uint8, device="cuda")
+    nonzero_in = torch.from_numpy(((dy & 0x7FFF) != 0).view(np.uint8)).cuda().view(t, fout // 2, 2)
+    flush = {"tensor": "gpt6.7b qkv dY [16384, 12288]", "nonzero_elements": nz}
+    for name, mode, rht in (("nr", mx.MX_MODE_NR, False), ("sr", mx.MX_MODE_SR, False),
+                            ("rht_nr", mx.MX_MODE_RHT_NR, True), ("rht_sr", mx.MX_MODE_RHT_SR, True)):
+        mx.mx_quantize(ddy, codes, scales, 64, 0x0F27_0000_0000_0000, mode)
+        z = torch.stack([(codes & 7) == 0, ((codes >> 4) & 7) == 0], dim=-1)
+        if rht:
+            frac = float(z.sum().item()) / (t * fout)
+        else:
+            frac = float((z & nonzero_in.bool()).sum().item()) / nz
+        flush[name] = frac
+    # oracle's expected flush fraction (SR modes) on the first rows
+    ids = np.arange(256)
+    for name, rht in (("sr", False), ("rht_sr", True)):
+        _, _, pz = oracle.sr_moments(dy[ids], 64, 0x0F27_0000_0000_0000, rht)
+        mask = np.ones_like(pz, dtype=bool) if rht else (dy[ids] & 0x7FFF) != 0
+        flush[name + "_oracle_first_256_rows"] = float(pz[mask].sum() / mask.sum())
+    print(f"[var] flush to zero: {flush}", file=sys.stderr, flush=True)
+    return {"variance": rows, "flush_to_zero": flush}
 
 
 def gemm_baselines(torch, layers, reps=10):
@@ -767,6 +858,9 @@ def main():
         return
     if args.rht_overhead:
         print(json.dumps({"rht_overhead": rht_overhead(torch, mx)}))
+        return
+    if args.rht_variance:
+        print(json.dumps({"rht_variance": rht_variance(torch, mx)}))
         return
     config = args.config
     t0 = time.perf_counter()
