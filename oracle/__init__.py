@@ -29,7 +29,7 @@ Every reading taken where the paper is silent or garbled is listed in the
 docstring of the function that takes it.
 """
 
-from .philox import philox4x32_10, philox4x32_10_scalar, sign_vector, noise16
+from .philox import philox4x32_10, philox4x32_10_scalar, sign_vector, noise16, noise8
 from .formats import E2M1_VALUES, e2m1_value, e8m0_value
 from .hadamard import sylvester, hadamard_fp32, rht_fp32
 from .mxquant import (shared_exponent_byte, mx_normalize, sr_e2m1, quantize_rht_sr,
@@ -39,7 +39,7 @@ from .backward import linear_backward, bias_grad, linear_backward_accumulate
 from .variance import sr_moments, estimator_alpha, inner_product_variance, expected_zero_codes
 
 __all__ = [
-    "philox4x32_10", "philox4x32_10_scalar", "sign_vector", "noise16",
+    "philox4x32_10", "philox4x32_10_scalar", "sign_vector", "noise16", "noise8",
     "E2M1_VALUES", "e2m1_value", "e8m0_value",
     "sylvester", "hadamard_fp32", "rht_fp32",
     "shared_exponent_byte", "mx_normalize", "sr_e2m1", "quantize_rht_sr", "quantize_nr",

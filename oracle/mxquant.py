@@ -26,13 +26,17 @@ Readings (the paper is silent on each):
   magnitude rounds up iff floor(t * 2^16) + r >= 2^16, which happens with
   probability floor(t * 2^16) / 2^16. The sign is kept, except that a zero
   magnitude always gets the code 0 (no negative zero).
+* Cheaper-noise variant (a documented change of the rule above, selected
+  explicitly, never the default): 8 bits, round up iff
+  floor(t * 2^8) + r >= 2^8, probability floor(t * 2^8) / 2^8; its bias is at
+  most 2^-8 of the grid step instead of 2^-16 (noise layout in ``philox``).
 """
 
 import numpy as np
 
 from .formats import E2M1_VALUES, E2M1_EMAX, E2M1_MAX, MX_BLOCK, E8M0_BIAS, E8M0_NAN
 from .hadamard import rht_fp32
-from .philox import sign_vector, noise16
+from .philox import sign_vector, noise16, noise8
 
 SR_BITS = 16
 
@@ -59,11 +63,14 @@ def shared_exponent_byte(amax):
     return np.where(finite, byte, E8M0_NAN).astype(np.uint8)
 
 
-def sr_e2m1(w, r16):
-    """Stochastic rounding of float32 values |w| < 6 to E2M1 codes, with 16-bit noise r16.
+def sr_e2m1(w, r16, bits=SR_BITS):
+    """Stochastic rounding of float32 values |w| < 6 to E2M1 codes, with
+    ``bits``-bit noise r16 (16, the method's rule; 8, the cheaper variant).
 
     Returns uint8 codes 0..15 (bit 3 = sign, bits 0..2 = index into the grid).
     """
+    if bits not in (8, 16):
+        raise ValueError("noise bits must be 16 or 8")
     w = np.asarray(w, dtype=np.float32)
     r16 = np.asarray(r16, dtype=np.int64)
     a = np.abs(w.astype(np.float64))
@@ -73,8 +80,8 @@ def sr_e2m1(w, r16):
     f = E2M1_VALUES[idx]
     step = E2M1_VALUES[idx + 1] - f
     t = (a - f) / step                                            # exact in float64
-    t16 = np.floor(t * 2.0 ** SR_BITS).astype(np.int64)
-    up = (t16 + r16) >= 2 ** SR_BITS
+    tq = np.floor(t * 2.0 ** bits).astype(np.int64)
+    up = (tq + r16) >= 2 ** bits
     mag = idx + up.astype(np.int64)
     neg = np.signbit(w) & (mag != 0)
     return (mag | np.where(neg, 8, 0)).astype(np.uint8)
@@ -108,7 +115,7 @@ def mx_normalize(y):
     return scales, w
 
 
-def quantize_rht_sr(x_bits, g, seed, row_ids=None, rht=True):
+def quantize_rht_sr(x_bits, g, seed, row_ids=None, rht=True, noise_bits=SR_BITS):
     """Blockwise RHT followed by Algorithm 2, on a logical [rows, cols] bf16 matrix.
 
     x_bits : uint16 bf16 bit patterns, the logical matrix (MX and RHT blocks run
@@ -117,6 +124,8 @@ def quantize_rht_sr(x_bits, g, seed, row_ids=None, rht=True):
     g      : RHT block size (32 | g, g <= 256, power of two).
     seed   : 64-bit seed (hi32 selects the sign vector, all 64 bits the noise).
     rht    : False skips the transform (the "SR only" ablation of Table 2).
+    noise_bits : 16 (the method) or 8 (the cheaper-noise variant; needs
+             64 | cols).
 
     Returns (codes, scales): codes uint8 [rows, cols] one 4-bit code per element,
     scales uint8 [rows, cols/32] E8M0 bytes.
@@ -133,8 +142,10 @@ def quantize_rht_sr(x_bits, g, seed, row_ids=None, rht=True):
     scales, w = mx_normalize(y)
     if row_ids is not None and len(row_ids) != rows:
         raise ValueError("row_ids must name every row of x_bits")
-    r16 = noise16(seed, rows, cols, row_ids)
-    codes = sr_e2m1(w, r16)
+    if noise_bits == 8:
+        codes = sr_e2m1(w, noise8(seed, rows, cols, row_ids), bits=8)
+    else:
+        codes = sr_e2m1(w, noise16(seed, rows, cols, row_ids))
     return codes, scales
 
 

@@ -23,6 +23,12 @@ Readings (the paper is silent on all of them):
   hi32(L >> 3), 0, 0); output word (L >> 1) & 3; the element takes the low 16
   bits of that word if L is even, the high 16 bits if L is odd. So one
   generator call serves 8 consecutive elements of a row.
+* 8-bit noise (the cheaper-noise variant, a documented change of the rounding
+  rule, not the method's default): element (r, c) with c = 64 a + 32 h + 8 b + e
+  (h in {0, 1}, b in 0..3, e in 0..7) takes byte k = 8 h + e, i.e. byte k & 3 of
+  output word k >> 2, of Philox(counter = (lo32(P), hi32(P), 0, 0), key as
+  above) with P = (r * cols + 64 a + 8 b) >> 3. So one generator call serves 16
+  elements: the 8 at 64 a + 8 b and the 8 thirty-two columns further.
 """
 
 import numpy as np
@@ -103,4 +109,25 @@ def noise16(seed, rows, cols, row_ids=None):
     for i in range(4):                      # word i serves elements 2i (low half) and 2i+1 (high half)
         out[:, :, 2 * i] = w[i] & np.uint32(0xFFFF)
         out[:, :, 2 * i + 1] = w[i] >> np.uint32(16)
+    return out.reshape(len(r), cols)
+
+
+def noise8(seed, rows, cols, row_ids=None):
+    """8-bit dithering noise (the cheaper-noise variant) for each element of a
+    logical [rows, cols] matrix, cols a multiple of 64; ``row_ids`` as for
+    noise16. Returns uint32 values in [0, 256)."""
+    if cols % 64:
+        raise ValueError("cols must be a multiple of 64")
+    lo, hi = _split(seed)
+    r = np.arange(rows, dtype=np.uint64) if row_ids is None else np.asarray(row_ids, dtype=np.uint64)
+    n64 = cols // 64
+    a = np.arange(n64, dtype=np.uint64)[None, :, None]
+    b = np.arange(4, dtype=np.uint64)[None, None, :]
+    p = r[:, None, None] * np.uint64(cols // 8) + np.uint64(8) * a + b          # [rows, n64, 4]
+    w = philox4x32_10(p & np.uint64(MASK32), p >> np.uint64(32), 0, 0, lo, hi)
+    out = np.empty((len(r), n64, 2, 4, 8), dtype=np.uint32)                   # [row, a, h, b, e]
+    for h in range(2):
+        for e in range(8):
+            k = 8 * h + e
+            out[:, :, h, :, e] = (w[k >> 2] >> np.uint32(8 * (k & 3))) & np.uint32(0xFF)
     return out.reshape(len(r), cols)

@@ -41,7 +41,7 @@ from .mxquant import SR_BITS, bf16_bits_to_fp32, mx_normalize
 from .philox import sign_vector
 
 
-def sr_moments(x_bits, g, seed, rht=True):
+def sr_moments(x_bits, g, seed, rht=True, noise_bits=SR_BITS):
     """Per element of a logical [rows, cols] bf16 matrix quantised as
     ``quantize_rht_sr(x_bits, g, seed, rht=rht)`` does: (E[q], E[q^2], P(code 0))
     over the rounding noise, in float64, with q the dequantised value (E2M1
@@ -57,7 +57,7 @@ def sr_moments(x_bits, g, seed, rht=True):
     f = E2M1_VALUES[idx]
     c = E2M1_VALUES[np.minimum(idx + 1, len(E2M1_VALUES) - 1)]
     t = np.where(c > f, (a - f) / np.where(c > f, c - f, 1.0), 0.0)
-    p_up = np.floor(t * 2.0 ** SR_BITS) / 2.0 ** SR_BITS
+    p_up = np.floor(t * 2.0 ** noise_bits) / 2.0 ** noise_bits
     xs = np.ldexp(1.0, scales.astype(np.int64) - E8M0_BIAS).repeat(32, axis=1)
     sgn = np.where(np.signbit(w), -1.0, 1.0)
     mean = sgn * (f + p_up * (c - f)) * xs
