@@ -186,16 +186,17 @@ def input_sets(layers):
     return sets, per_set
 
 
-def step_ex(torch, mx, layers, g, flags, with_db):
+def step_ex(torch, mx, layers, g, flags, with_db, mode=None):
     """The step through mx_linear_backward_ex (bf16 dX buffers, db buffers made
-    on first use; dW is accumulated into when flags say so)."""
+    on first use; dW is accumulated into when flags say so), in quantiser mode
+    `mode` (default: the method, MX_MODE_RHT_SR)."""
+    mode = mx.MX_MODE_RHT_SR if mode is None else mode
     for L in layers:
         if not hasattr(L, "dx16"):
             L.dx16 = torch.empty((L.t, L.fin), dtype=torch.int16, device="cuda")
             L.db = torch.zeros(L.fout, dtype=torch.float32, device="cuda")
         dx = L.dx16 if flags & mx.MX_BWD_DX_BF16 else L.dx
-        mx.mx_linear_backward_ex(L.dy, L.x, L.w, dx, L.dw, L.db if with_db else None, g, SEED,
-                                 mx.MX_MODE_RHT_SR, flags)
+        mx.mx_linear_backward_ex(L.dy, L.x, L.w, dx, L.dw, L.db if with_db else None, g, SEED, mode, flags)
 
 
 def variants(torch, mx, sets, g, steps, warmup, rounds=3):
@@ -204,26 +205,29 @@ def variants(torch, mx, sets, g, steps, warmup, rounds=3):
     rounds is reported, so that clock drift does not favour any kind. Steps
     rotate through the input sets as the headline step does."""
     bf, acc = mx.MX_BWD_DX_BF16, mx.MX_BWD_ACCUMULATE
-    kinds = (("plain", None, False), ("ex_no_options", 0, False), ("bf16_dx", bf, False),
-             ("bias_grad", 0, True), ("bf16_dx_accumulate_bias_grad", bf | acc, True))
+    # (name, flags, db, mode): the framework options, and the method with the
+    # cheaper 8-bit dither (a different rounding rule, reported beside it)
+    kinds = (("plain", None, False, None), ("ex_no_options", 0, False, None), ("bf16_dx", bf, False, None),
+             ("bias_grad", 0, True, None), ("bf16_dx_accumulate_bias_grad", bf | acc, True, None),
+             ("rht_sr8_noise", 0, False, mx.MX_MODE_RHT_SR8))
 
-    def run(flags, with_db, n):
+    def run(flags, with_db, mode, n):
         for i in range(n):
             layers = sets[i % len(sets)]
             if flags is None:
                 step(mx, layers, g)
             else:
-                step_ex(torch, mx, layers, g, flags, with_db)
+                step_ex(torch, mx, layers, g, flags, with_db, mode)
 
-    for _, flags, with_db in kinds:
-        run(flags, with_db, warmup)
-    times = {name: [] for name, _, _ in kinds}
+    for _, flags, with_db, mode in kinds:
+        run(flags, with_db, mode, warmup)
+    times = {name: [] for name, _, _, _ in kinds}
     for _ in range(rounds):
-        for name, flags, with_db in kinds:
+        for name, flags, with_db, mode in kinds:
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            run(flags, with_db, steps)
+            run(flags, with_db, mode, steps)
             e1.record()
             torch.cuda.synchronize()
             times[name].append(e0.elapsed_time(e1) / steps)

@@ -96,7 +96,8 @@ enum mx_status {
 };
 
 /*
- * Quantiser modes: the method and the ablation rows of Table 2.
+ * Quantiser modes: the method, the ablation rows of Table 2, and a
+ * cheaper-noise variant.
  *   MX_MODE_RHT_SR  blockwise RHT, then Algorithm 2 (3/4 pre-scale, stochastic
  *                   rounding): the method, and what the entry points without a
  *                   mode argument use.
@@ -105,12 +106,22 @@ enum mx_status {
  *                   (exact), rounded to the nearest E2M1 value (ties to the even
  *                   code), saturating at 6.
  *   MX_MODE_NR      Algorithm 1 alone: the plain OCP MX conversion.
+ *   MX_MODE_RHT_SR8 MX_MODE_RHT_SR with a cheaper dither, a deliberate change
+ *                   of the rounding rule above (never a default): 8 noise
+ *                   bits, |w| rounds up iff floor(t * 2^8) + r >= 2^8 (bias at
+ *                   most 2^-8 of the grid step instead of 2^-16). Element
+ *                   (r, c) of the logical matrix, c = 64 a + 32 h + 8 b + e
+ *                   (h < 2, b < 4, e < 8), takes byte (8 h + e) & 3 of word
+ *                   (8 h + e) >> 2 of Philox(counter = (lo32(P), hi32(P), 0, 0),
+ *                   key = (lo32(seed), hi32(seed))), P = (r * cols + 64 a + 8 b)
+ *                   >> 3: one generator call per 16 elements instead of 8.
+ *                   Needs g in {64, 128, 256} (MX_ERR_G otherwise).
  * The E8M0 scale rule, code layout, canonical zero and non-finite handling are
  * the same in every mode. Modes without the RHT ignore g (their blocks are the
  * 32-element MX blocks) and hi32(seed); modes with round to nearest ignore
  * lo32(seed).
  */
-enum mx_mode { MX_MODE_RHT_SR = 0, MX_MODE_SR = 1, MX_MODE_RHT_NR = 2, MX_MODE_NR = 3 };
+enum mx_mode { MX_MODE_RHT_SR = 0, MX_MODE_SR = 1, MX_MODE_RHT_NR = 2, MX_MODE_NR = 3, MX_MODE_RHT_SR8 = 4 };
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char* mx_status_string(int status);

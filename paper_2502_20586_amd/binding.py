@@ -24,6 +24,8 @@ MX_NOALLOC_SCRATCH_BYTES = 64 << 20
 # Quantiser modes (include/mxfp4.h, enum mx_mode): the method and the ablation
 # rows of Table 2.
 MX_MODE_RHT_SR, MX_MODE_SR, MX_MODE_RHT_NR, MX_MODE_NR = 0, 1, 2, 3
+# The cheaper-noise variant (8-bit dither; a deliberate change of the rounding rule).
+MX_MODE_RHT_SR8 = 4
 
 # Options of mx_linear_backward_ex (include/mxfp4.h, enum mx_backward_flags).
 MX_BWD_DX_BF16, MX_BWD_ACCUMULATE = 1, 2

@@ -162,9 +162,12 @@ int scratch_for_device(void** out) {
 bool valid_g(int g) { return g == 32 || g == 64 || g == 128 || g == 256; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-bool valid_mode(int mode) { return mode >= MX_MODE_RHT_SR && mode <= MX_MODE_NR; }
-bool mode_has_rht(int mode) { return mode == MX_MODE_RHT_SR || mode == MX_MODE_RHT_NR; }
-bool mode_has_sr(int mode) { return mode == MX_MODE_RHT_SR || mode == MX_MODE_SR; }
+bool valid_mode(int mode) { return mode >= MX_MODE_RHT_SR && mode <= MX_MODE_RHT_SR8; }
+bool mode_has_rht(int mode) { return mode == MX_MODE_RHT_SR || mode == MX_MODE_RHT_NR || mode == MX_MODE_RHT_SR8; }
+bool mode_has_sr(int mode) { return mode == MX_MODE_RHT_SR || mode == MX_MODE_SR || mode == MX_MODE_RHT_SR8; }
+// g accepted by a mode with the RHT: 8-bit noise serves two 32-element chunks
+// of a lane per generator call, so it needs g >= 64.
+bool valid_g_for(int mode, int g) { return valid_g(g) && (mode != MX_MODE_RHT_SR8 || g >= 64); }
 // Block along the reduction dimension that a mode needs whole: g with the
 // RHT, the 32-element MX block without it (g is then ignored).
 int mode_block(int mode, int g) { return mode_has_rht(mode) ? g : 32; }
@@ -172,7 +175,7 @@ int mode_block(int mode, int g) { return mode_has_rht(mode) ? g : 32; }
 int validate_quant(const uint16_t* in, const uint8_t* codes, const uint8_t* scales, int64_t rows,
                    int64_t cols, int g, bool transposed, int mode) {
   if (!valid_mode(mode)) return MX_ERR_MODE;
-  if (mode_has_rht(mode) && !valid_g(g)) return MX_ERR_G;
+  if (mode_has_rht(mode) && !valid_g_for(mode, g)) return MX_ERR_G;
   if (rows < 0 || cols < 0 || cols % mode_block(mode, g) != 0) return MX_ERR_SHAPE;
   if (rows == 0 || cols == 0) return MX_OK;
   if (!in || !codes || !scales) return MX_ERR_NULL;
@@ -229,7 +232,7 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
                     unsigned flags, hipStream_t s, bool noalloc = false) {
   if (!valid_mode(mode)) return MX_ERR_MODE;
   if (flags & ~kKnownFlags) return MX_ERR_FLAGS;
-  if (mode_has_rht(mode) && !valid_g(g)) return MX_ERR_G;
+  if (mode_has_rht(mode) && !valid_g_for(mode, g)) return MX_ERR_G;
   const int blk = mode_block(mode, g);
   if (T < 0 || in_features < 0 || out_features < 0 || T % blk != 0 || out_features % blk != 0 ||
       in_features >= mx::kGemmMaxN)
@@ -425,7 +428,7 @@ int mx_linear_backward_ex(const uint16_t* dY, const uint16_t* X, const uint16_t*
 int64_t mx_linear_backward_ex_workspace_bytes(int64_t T, int64_t in_features, int64_t out_features, int g,
                                               int mode, int with_db) {
   if (T < 0 || in_features < 0 || out_features < 0 || !valid_mode(mode)) return 0;
-  if (mode_has_rht(mode) && !valid_g(g)) return 0;
+  if (mode_has_rht(mode) && !valid_g_for(mode, g)) return 0;
   const int64_t colsum_bytes = with_db ? T / mode_block(mode, g) * out_features * 4 : 0;
   return layout_workspace(T, in_features, out_features, nullptr, nullptr, nullptr, colsum_bytes);
 }

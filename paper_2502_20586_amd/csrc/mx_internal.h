@@ -34,9 +34,9 @@ struct QuantSpec {
   float* colsum = nullptr;
 };
 
-// The paper's quantiser and its ablations (Table 1 rows); values match the
-// C ABI's MX_MODE_* constants.
-enum class QuantMode : int { kRhtSr = 0, kSr = 1, kRhtNr = 2, kNr = 3 };
+// The paper's quantiser, its ablations (Table 2 rows) and the cheaper-noise
+// variant (8-bit dither); values match the C ABI's MX_MODE_* constants.
+enum class QuantMode : int { kRhtSr = 0, kSr = 1, kRhtNr = 2, kNr = 3, kRhtSr8 = 4 };
 
 // Up to 4 quantisations with the same g and mode in one launch. Modes without
 // the RHT ignore g (their blocks are the 32-element MX blocks).

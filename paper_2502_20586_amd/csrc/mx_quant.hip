@@ -175,11 +175,16 @@ __device__ __forceinline__ void sr_convert(const v2f (&w)[4], const uint32_t (&s
 
 // One MX block (chunk r of the quad): E8M0 scale, then 8 codes of this lane.
 // Returns the packed codes (element e in bits 4e..4e+3); *scale gets the byte.
-// SR: Algorithm 2 (3/4 pre-scale, stochastic rounding); otherwise Algorithm 1
-// (no 3/4, round to nearest with ties to the even code, saturation at 6).
-template <bool SR>
+// NB, the dither's noise bits: 16, Algorithm 2 (3/4 pre-scale, stochastic
+// rounding) with the 16-bit noise of the chunk's own Philox call; 8, the same
+// with the cheaper 8-bit noise, bytes 8 h .. 8 h + 7 of the call `rnd8` that
+// serves this chunk (h = 0) and the one 32 columns further (h = 1); 0,
+// Algorithm 1 (no 3/4, round to nearest with ties to the even code,
+// saturation at 6).
+template <int NB>
 __device__ __forceinline__ uint32_t quantise_chunk(const float (&y)[8], uint64_t chunk_index,
-                                                   uint32_t seed_lo, uint32_t seed_hi, uint32_t* scale) {
+                                                   uint32_t seed_lo, uint32_t seed_hi, uint32_t* scale,
+                                                   const Rand4& rnd8 = Rand4{}, int h = 0) {
   // Block maximum of |y| on the bit patterns. As unsigned integers, patterns
   // with the sign bit set sort above all others and among themselves by
   // magnitude; as signed integers, non-negative patterns sort by magnitude
@@ -205,7 +210,7 @@ __device__ __forceinline__ uint32_t quantise_chunk(const float (&y)[8], uint64_t
   // shared_exp = floor(log2 amax) - 2, as a biased E8M0 byte, clamped at 0.
   const uint32_t ebyte = max(efield, 2u) - 2u;
   uint32_t packed;
-  if constexpr (!SR) {
+  if constexpr (NB == 0) {
     // v = y / 2^shared_exp, an exact power-of-two scaling (finite blocks have
     // ebyte <= 252, so the factor is a normal float); the converter rounds to
     // nearest even and saturates.
@@ -218,17 +223,30 @@ __device__ __forceinline__ uint32_t quantise_chunk(const float (&y)[8], uint64_t
   } else {
     // c = (3/4) 2^-shared_exp = 1.5 * 2^(126 - ebyte): always a normal float.
     const float c = __uint_as_float(((253u - ebyte) << 23) | 0x400000u);
-    // Noise: word i of the chunk's Philox block serves elements 2i (low half)
-    // and 2i + 1 (high half).
-    const Rand4 rnd = philox4x32_10((uint32_t)chunk_index, (uint32_t)(chunk_index >> 32), 0, 0,
-                                    seed_lo, seed_hi);
     v2f w[4];
     uint32_t se[4], so[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      w[i] = v2f{y[2 * i] * c, y[2 * i + 1] * c};  // (3/4) y / X, one rounding each
-      se[i] = rnd.w[i] << 16;
-      so[i] = (rnd.w[i] >> 16) << 15;
+    for (int i = 0; i < 4; ++i) w[i] = v2f{y[2 * i] * c, y[2 * i + 1] * c};  // (3/4) y / X, one rounding each
+    if constexpr (NB == 16) {
+      // Noise: word i of the chunk's Philox block serves elements 2i (low
+      // half) and 2i + 1 (high half).
+      const Rand4 rnd = philox4x32_10((uint32_t)chunk_index, (uint32_t)(chunk_index >> 32), 0, 0,
+                                      seed_lo, seed_hi);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        se[i] = rnd.w[i] << 16;
+        so[i] = (rnd.w[i] >> 16) << 15;
+      }
+    } else {
+      // 8-bit noise: element e takes byte e & 3 of word 2 h + (e >> 2). With
+      // R = r << 14 the converter's rule floor(t 2^22) + R >= 2^22 is exactly
+      // floor(t 2^8) + r >= 2^8: seed r << 24 (first slot), r << 23 (second).
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t wd = h ? rnd8.w[2 + (i >> 1)] : rnd8.w[i >> 1];
+        se[i] = (i & 1) ? (wd << 8) & 0xFF000000u : wd << 24;
+        so[i] = (i & 1) ? (wd >> 1) & 0x7F800000u : (wd << 15) & 0x7F800000u;
+      }
     }
     // Byte i of `even` holds element 2i's code in its low nibble, byte i of
     // `odd` element 2i + 1's code in its high nibble.
@@ -300,9 +318,10 @@ __device__ __forceinline__ void store_chunk(const QuantJob& job, int64_t row, in
 // its (row, block-in-row) pair advances by the grid stride's quotient and
 // remainder, so no division runs inside the loop. For g <= 64 the next block's
 // loads are issued before the current block is quantised.
-template <int G, bool RHT, bool SR, bool KT>
+template <int G, bool RHT, int NB, bool KT>
 __device__ __forceinline__ void rows_body(const QuantJob& job, int64_t wg, int64_t nwg) {
   constexpr int NC = G / 32;
+  static_assert(NB != 8 || NC % 2 == 0, "8-bit noise pairs chunk r with chunk r + 1 (g >= 64)");
   constexpr bool kPrefetch = NC <= 2;
   const int q = threadIdx.x & 3;
   const uint32_t seed_lo = (uint32_t)job.seed, seed_hi = (uint32_t)(job.seed >> 32);
@@ -336,10 +355,15 @@ __device__ __forceinline__ void rows_body(const QuantJob& job, int64_t wg, int64
     if (RHT) butterfly<G>(v, q);
     const int64_t col0 = cb * G + q * 8;
     const uint64_t chunk0 = (uint64_t)(b * G + q * 8) >> 3;
+    Rand4 rnd8{};
 #pragma unroll
     for (int r = 0; r < NC; ++r) {
+      // 8-bit noise: one Philox call for chunks r and r + 1 (r even), the
+      // counter of chunk r's 16-bit draw.
+      if (NB == 8 && (r & 1) == 0)
+        rnd8 = philox4x32_10((uint32_t)(chunk0 + 4 * r), (uint32_t)((chunk0 + 4 * r) >> 32), 0, 0, seed_lo, seed_hi);
       uint32_t sbyte;
-      const uint32_t packed = quantise_chunk<SR>(v[r], chunk0 + 4 * r, seed_lo, seed_hi, &sbyte);
+      const uint32_t packed = quantise_chunk<NB>(v[r], chunk0 + 4 * r, seed_lo, seed_hi, &sbyte, rnd8, r & 1);
       store_chunk<KT>(job, row, col0 + r * 32, packed, sbyte, q == (r & 3));
     }
     b += stride;
@@ -411,10 +435,11 @@ struct ColsCfg {
 // (bf16, before the sign flip) over each g-block, in FP32: every lane sums its
 // g/4 values of a row in chunk-then-element order, the quad adds the four lane
 // sums as (q0 + q1) + (q2 + q3), and lane q stores row RPQ k + q's sum.
-template <int G, bool RHT, bool SR, bool KT, int RPQ, bool LW2, bool CS = false>
+template <int G, bool RHT, int NB, bool KT, int RPQ, bool LW2, bool CS = false>
 __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64_t nwg, uint8_t* smem) {
   using CC = ColsCfg<G>;
   constexpr int NC = G / 32;
+  static_assert(NB != 8 || NC % 2 == 0, "8-bit noise pairs chunk r with chunk r + 1 (g >= 64)");
   constexpr int NP = RPQ / 2;                  // row pairs per quad
   constexpr int TR = 16 * RPQ;                 // logical rows per tile
   constexpr bool kMaskRegs = G <= 128;
@@ -574,10 +599,15 @@ __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64
           const int lr = RPQ * k + 2 * p + i;          // row inside the tile
           const int64_t row = rt * TR + lr;
           const uint64_t chunk0 = (uint64_t)(row * cols + col0) >> 3;
+          Rand4 rnd8{};
 #pragma unroll
           for (int r = 0; r < NC; ++r) {
+            if (NB == 8 && (r & 1) == 0)
+              rnd8 = philox4x32_10((uint32_t)(chunk0 + 4 * r), (uint32_t)((chunk0 + 4 * r) >> 32), 0, 0, seed_lo,
+                                   seed_hi);
             uint32_t sbyte;
-            const uint32_t packed = quantise_chunk<SR>(v[i][r], chunk0 + 4 * r, seed_lo, seed_hi, &sbyte);
+            const uint32_t packed =
+                quantise_chunk<NB>(v[i][r], chunk0 + 4 * r, seed_lo, seed_hi, &sbyte, rnd8, r & 1);
             const int unit = wave * NC + r;            // 16-byte code unit of this chunk in the staged row
             *reinterpret_cast<uint32_t*>(codes_lds + lr * CC::kCodeRow + ((unit ^ (k & CC::kSwz)) << 4) + 4 * q) =
                 packed;
@@ -645,7 +675,7 @@ __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64
 // so that the extra registers of that path do not cost the others occupancy).
 // g <= 64 fits 128 VGPRs: four waves per SIMD to hide the loads' latency
 // behind the VALU work of the others.
-template <int G, bool RHT, bool SR, bool KT, bool CS>
+template <int G, bool RHT, int NB, bool KT, bool CS>
 __global__ __launch_bounds__(kThreads, G <= 64 ? 4 : 1) void quant_kernel(QuantJobs jobs) {
   extern __shared__ __align__(16) uint8_t smem[];
   int j = 0;
@@ -656,27 +686,28 @@ __global__ __launch_bounds__(kThreads, G <= 64 ? 4 : 1) void quant_kernel(QuantJ
   const int64_t wg = (int64_t)blockIdx.x - job.wg_begin;
   const int64_t nwg = job.wg_end - job.wg_begin;
   if (!job.transposed)
-    rows_body<G, RHT, SR, KT>(job, wg, nwg);
+    rows_body<G, RHT, NB, KT>(job, wg, nwg);
   else if (CS && job.colsum)   // launch_jobs_g admits colsum jobs only at load_rows == kRpqMax
-    cols_body<G, RHT, SR, KT, ColsCfg<G>::kRpqMax, true, CS>(job, wg, nwg, smem);
+    cols_body<G, RHT, NB, KT, ColsCfg<G>::kRpqMax, true, CS>(job, wg, nwg, smem);
   else if (job.load_rows == 4)
-    cols_body<G, RHT, SR, KT, ColsCfg<G>::kRpqMax, true>(job, wg, nwg, smem);
+    cols_body<G, RHT, NB, KT, ColsCfg<G>::kRpqMax, true>(job, wg, nwg, smem);
   else if (job.load_rows == 2)
-    cols_body<G, RHT, SR, KT, 2, true>(job, wg, nwg, smem);
+    cols_body<G, RHT, NB, KT, 2, true>(job, wg, nwg, smem);
   else
-    cols_body<G, RHT, SR, KT, 2, false>(job, wg, nwg, smem);
+    cols_body<G, RHT, NB, KT, 2, false>(job, wg, nwg, smem);
 }
 
-// Kernel names for tracing: g-block size, "_nr" for round to nearest; "sr" /
-// "nr" alone without the RHT.
-template <int G, bool RHT, bool SR>
+// Kernel names for tracing: g-block size, "_nr" for round to nearest, "_sr8"
+// for 8-bit noise; "sr" / "nr" alone without the RHT.
+template <int G, bool RHT, int NB>
 const char* quant_name() {
-  if (!RHT) return SR ? "quant_sr" : "quant_nr";
-  if (SR) return G == 32 ? "quant_g32" : G == 64 ? "quant_g64" : G == 128 ? "quant_g128" : "quant_g256";
+  if (!RHT) return NB ? "quant_sr" : "quant_nr";
+  if (NB == 16) return G == 32 ? "quant_g32" : G == 64 ? "quant_g64" : G == 128 ? "quant_g128" : "quant_g256";
+  if (NB == 8) return G == 64 ? "quant_g64_sr8" : G == 128 ? "quant_g128_sr8" : "quant_g256_sr8";
   return G == 32 ? "quant_g32_nr" : G == 64 ? "quant_g64_nr" : G == 128 ? "quant_g128_nr" : "quant_g256_nr";
 }
 
-template <int G, bool RHT, bool SR, bool KT>
+template <int G, bool RHT, int NB, bool KT>
 int launch_jobs_g(QuantJobs jobs, hipStream_t stream) {
   constexpr int64_t kMaxWgPerJob = 256 * 8;
   int wg = 0;
@@ -701,40 +732,51 @@ int launch_jobs_g(QuantJobs jobs, hipStream_t stream) {
   if (wg == 0) return 0;
   double bytes = 0;
   for (int i = 0; i < jobs.count; ++i) bytes += (double)jobs.j[i].rows * jobs.j[i].cols * (2.0 + 0.5 + 1.0 / 32);
-  TraceScope trace(quant_name<G, RHT, SR>(), bytes, false);
+  TraceScope trace(quant_name<G, RHT, NB>(), bytes, false);
   bool any_t = false;
   for (int i = 0; i < jobs.count; ++i) any_t = any_t || jobs.j[i].transposed;
   bool any_cs = false;
   for (int i = 0; i < jobs.count; ++i) any_cs = any_cs || jobs.j[i].colsum != nullptr;
   const int lds = any_t ? ColsCfg<G>::kLds : 0;
   if (any_cs)
-    hipExtLaunchKernelGGL((quant_kernel<G, RHT, SR, KT, true>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
+    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, true>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
                           trace.start(), trace.stop(), 0, jobs);
   else
-    hipExtLaunchKernelGGL((quant_kernel<G, RHT, SR, KT, false>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
+    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, false>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
                           trace.start(), trace.stop(), 0, jobs);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
-template <bool RHT, bool SR, bool KT>
+template <bool RHT, int NB, bool KT>
 int launch_jobs_mode(const QuantJobs& jobs, int g, hipStream_t stream) {
-  if (!RHT) return launch_jobs_g<32, false, SR, KT>(jobs, stream);   // MX blocks of 32, no g-blocks
-  switch (g) {
-    case 32: return launch_jobs_g<32, true, SR, KT>(jobs, stream);
-    case 64: return launch_jobs_g<64, true, SR, KT>(jobs, stream);
-    case 128: return launch_jobs_g<128, true, SR, KT>(jobs, stream);
-    case 256: return launch_jobs_g<256, true, SR, KT>(jobs, stream);
-    default: return -1;
+  if constexpr (!RHT) {
+    return launch_jobs_g<32, false, NB, KT>(jobs, stream);   // MX blocks of 32, no g-blocks
+  } else if constexpr (NB == 8) {
+    switch (g) {   // pairs of 32-element chunks: g >= 64
+      case 64: return launch_jobs_g<64, true, 8, KT>(jobs, stream);
+      case 128: return launch_jobs_g<128, true, 8, KT>(jobs, stream);
+      case 256: return launch_jobs_g<256, true, 8, KT>(jobs, stream);
+      default: return -1;
+    }
+  } else {
+    switch (g) {
+      case 32: return launch_jobs_g<32, true, NB, KT>(jobs, stream);
+      case 64: return launch_jobs_g<64, true, NB, KT>(jobs, stream);
+      case 128: return launch_jobs_g<128, true, NB, KT>(jobs, stream);
+      case 256: return launch_jobs_g<256, true, NB, KT>(jobs, stream);
+      default: return -1;
+    }
   }
 }
 
 template <bool KT>
 int launch_jobs_kt(const QuantJobs& jobs, int g, QuantMode mode, hipStream_t stream) {
   switch (mode) {
-    case QuantMode::kRhtSr: return launch_jobs_mode<true, true, KT>(jobs, g, stream);
-    case QuantMode::kSr: return launch_jobs_mode<false, true, KT>(jobs, g, stream);
-    case QuantMode::kRhtNr: return launch_jobs_mode<true, false, KT>(jobs, g, stream);
-    case QuantMode::kNr: return launch_jobs_mode<false, false, KT>(jobs, g, stream);
+    case QuantMode::kRhtSr: return launch_jobs_mode<true, 16, KT>(jobs, g, stream);
+    case QuantMode::kSr: return launch_jobs_mode<false, 16, KT>(jobs, g, stream);
+    case QuantMode::kRhtNr: return launch_jobs_mode<true, 0, KT>(jobs, g, stream);
+    case QuantMode::kNr: return launch_jobs_mode<false, 0, KT>(jobs, g, stream);
+    case QuantMode::kRhtSr8: return launch_jobs_mode<true, 8, KT>(jobs, g, stream);
   }
   return -1;
 }

@@ -74,8 +74,12 @@ def test_quantize_modes_validation():
     need only cols % 32 == 0."""
     lib = _lib()
     q = lib.mx_quantize
-    for mode in (-1, 4, 99):
+    for mode in (-1, 5, 99):
         assert q(FAKE, FAKE, FAKE, 4, 64, 64, 0, mode, 0, None) == -8
+    # the 8-bit-noise variant pairs 32-element chunks: g = 32 is refused
+    assert q(FAKE, FAKE, FAKE, 4, 64, 32, 0, binding.MX_MODE_RHT_SR8, 0, None) == -2
+    assert lib.mx_linear_backward_mode(FAKE, FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 32, 0,
+                                       binding.MX_MODE_RHT_SR8, None) == -2
     assert q(FAKE, FAKE, FAKE, 4, 64, 48, 0, binding.MX_MODE_RHT_NR, 0, None) == -2   # g checked with RHT
     assert q(FAKE, FAKE, FAKE, 4, 96, 64, 0, binding.MX_MODE_RHT_NR, 1, None) == -3   # cols % g
     for mode in (binding.MX_MODE_SR, binding.MX_MODE_NR):

@@ -128,7 +128,7 @@ def test_backward_ex_without_options_is_mx_linear_backward():
         assert np.array_equal(dx, host(dx0)) and np.array_equal(dw, host(dw0))
 
 
-@pytest.mark.parametrize("mode", [1, 2, 3])
+@pytest.mark.parametrize("mode", [1, 2, 3, 4])
 def test_backward_ex_db_in_every_mode(mode):
     """Modes without the RHT sum dY in 32-element blocks, the RHT modes in g-blocks:
     db is the same column sum either way (within its bound)."""

@@ -7,6 +7,8 @@ mx_linear_backward_mode.
   the even code, saturation at 6) after / without the RHT; the oracle is
   quantize_nr, which raises on non-finite input, so these modes are checked on
   finite data only.
+* MX_MODE_RHT_SR8: the cheaper-noise variant (8-bit dither); the oracle is
+  quantize_rht_sr with noise_bits=8.
 
 Codes and scales must match bit for bit; GEMM outputs within normwise relative
 error 1e-5 of the oracle's FP64 product with the mode's rescale.
@@ -23,7 +25,7 @@ from gpu_util import torch_gpu, to_dev, empty_u8, host, note, rel_err
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-5
-RHT_SR, SR, RHT_NR, NR = 0, 1, 2, 3
+RHT_SR, SR, RHT_NR, NR, RHT_SR8 = 0, 1, 2, 3, 4
 SEEDS = [0, 0x0123456789ABCDEF, 0xFFFFFFFFFFFFFFFF]
 
 
@@ -32,6 +34,8 @@ def oracle_quant(bits, g, seed, mode):
         return oracle.quantize_rht_sr(bits, g, seed)
     if mode == SR:
         return oracle.quantize_rht_sr(bits, 32, seed, rht=False)
+    if mode == RHT_SR8:
+        return oracle.quantize_rht_sr(bits, g, seed, noise_bits=8)
     signs = oracle.sign_vector(seed, g) if mode == RHT_NR else None
     codes, scales, _ = oracle.quantize_nr(bf16_bits_to_fp32(bits), rht_signs=signs)
     return codes, scales
@@ -58,7 +62,7 @@ def _check(bits, g, seed, mode, transposed):
 
 @pytest.mark.parametrize("transposed", [False, True])
 @pytest.mark.parametrize("mode,g", [(SR, 64), (NR, 64), (RHT_NR, 32), (RHT_NR, 64), (RHT_NR, 128),
-                                    (RHT_NR, 256)])
+                                    (RHT_NR, 256), (RHT_SR8, 64), (RHT_SR8, 128), (RHT_SR8, 256)])
 def test_modes_small_ragged(mode, g, transposed):
     # several quad groups and tiles, plus rows not a multiple of 16 or 64
     for rows, mult in ((1, 1), (37, 3), (130, 2), (64, 4)):
@@ -92,13 +96,13 @@ def test_nearest_rounding_ties_and_saturation():
         _check(bits, 64, 0, NR, transposed)
 
 
-@pytest.mark.parametrize("mode", [RHT_SR, SR, RHT_NR, NR])
+@pytest.mark.parametrize("mode", [RHT_SR, SR, RHT_NR, NR, RHT_SR8])
 def test_linear_backward_modes(mode):
     """dX = alpha Q0 Q1^T and dW = alpha Q2 Q3^T with each operand quantised in
     `mode` (seed ^ i), alpha = (16/9 with SR) / (g with the RHT)."""
     torch = torch_gpu()
     import paper_2502_20586_amd as mx
-    for t, fin, fout, g in ((256, 96, 512, 64), (128, 72, 256, 128), (512, 200, 384, 32)):
+    for t, fin, fout, g in ((256, 96, 512, 64), (128, 72, 256, 128), (512, 200, 384, 64 if mode == RHT_SR8 else 32)):
         dy = matrix((t, fout), seed=[t, mode, 1], dist="t3", scale=1e-3, outlier_p=0.01, outlier_factor=100.0)
         x = matrix((t, fin), seed=[t, mode, 2])
         w = matrix((fout, fin), seed=[t, mode, 3], scale=0.02)
@@ -107,7 +111,7 @@ def test_linear_backward_modes(mode):
         dx = torch.full((t, fin), float("nan"), dtype=torch.float32, device="cuda")
         dw = torch.full((fout, fin), float("nan"), dtype=torch.float32, device="cuda")
         mx.mx_linear_backward_mode(to_dev(dy), to_dev(x), to_dev(w), dx, dw, g, seed, mode)
-        alpha = (16.0 / 9.0 if mode in (RHT_SR, SR) else 1.0) / (g if mode in (RHT_SR, RHT_NR) else 1)
+        alpha = (16.0 / 9.0 if mode in (RHT_SR, SR, RHT_SR8) else 1.0) / (g if mode in (RHT_SR, RHT_NR, RHT_SR8) else 1)
         q0 = oracle_quant(dy, g, seed ^ 0, mode)
         q1 = oracle_quant(np.ascontiguousarray(w.T), g, seed ^ 1, mode)
         q2 = oracle_quant(np.ascontiguousarray(dy.T), g, seed ^ 2, mode)
