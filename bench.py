@@ -917,7 +917,7 @@ def main():
         "quantize_gbs": quant_bytes / (quant_ms * 1e-3) / 1e9,
         "quantize_ms_per_step": quant_ms / args.steps,
         "gemm_ms_per_step": gemm_ms / args.steps,
-        "gemm_tflops": flops / (gemm_ms * 1e-3) / 1e12,
+        "gemm_tflops": flops * args.steps / (gemm_ms * 1e-3) / 1e12,
         "mfma_peak_frac": value / MXFP4_PEAK_TFLOPS,
         "roofline": roof,
         "quantize_roofline": roofline_of(config, prof, qk, args.steps) if qk else None,
