@@ -142,6 +142,11 @@ class Layer:
     def flops(self):
         return 4 * self.t * self.fin * self.fout
 
+    def quant_elements(self):
+        """Elements of the four quantised operands: dY twice (along out and along
+        the tokens), W and x once each."""
+        return 2 * self.t * self.fout + self.fin * self.fout + self.fin * self.t
+
 
 def step(mx, layers, g):
     for L in layers:
@@ -653,9 +658,9 @@ def config_runs(torch, mx, steps=10, warmup=3):
         torch.cuda.synchronize()
         print(f"[configs] {config}: inputs ready in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
         flops = sum(L.flops() for L in layers)
-        qbytes = sum((2 * L.t * L.fout + L.fin * L.fout + L.fin * L.t) * QUANT_BYTES_PER_ELEM for L in layers)
         res = {"tokens": cfg["tokens"], "linears": [[n_, i_, o_] for n_, i_, o_ in cfg["linears"]],
-               "gemm_flops_per_step": flops, "quant_bytes_per_step": qbytes, "by_g": {}}
+               "gemm_flops_per_step": flops, "quant_elements_per_step": sum(L.quant_elements() for L in layers),
+               "by_g": {}}
         # Settle the clocks on this config's step before its first timing.
         warm_up(torch, lambda i: step(mx, layers, cfg["g"][0]), min_steps=warmup)
         for g in cfg["g"]:
@@ -675,10 +680,12 @@ def config_runs(torch, mx, steps=10, warmup=3):
             torch.cuda.synchronize()
             prof = mx.mx_profile_stop()
             q_ms = sum(v["total_ms"] for k, v in prof.items() if k.startswith("quant")) / steps
+            # algorithmic bytes as the library counts them (each input read once)
+            qbytes = sum(v["work"] for k, v in prof.items() if k.startswith("quant")) / steps
             g_ms = sum(v["total_ms"] for k, v in prof.items() if k.startswith("gemm") or k == "splitk_reduce") / steps
             res["by_g"][str(g)] = {
                 "ms_per_step": ms, "tflops": flops / (ms * 1e-3) / 1e12,
-                "quant_ms": q_ms, "quant_gbs": qbytes / (q_ms * 1e-3) / 1e9,
+                "quant_ms": q_ms, "quant_bytes_per_step": qbytes, "quant_gbs": qbytes / (q_ms * 1e-3) / 1e9,
                 "gemm_ms": g_ms, "gemm_tflops": flops / (g_ms * 1e-3) / 1e12,
                 "kernels": {k: {"avg_us": v["total_ms"] * 1e3 / v["launches"], "launches_per_step": v["launches"] / steps}
                             for k, v in prof.items()}}
@@ -819,10 +826,11 @@ def roofline_of(config, prof, kernel, steps):
     return roof
 
 
-def alu_roofline_of(config, prof, kernel):
+def alu_roofline_of(config, prof, kernel, elems_per_step, steps):
     """The quantiser is bound by vector ALU issue, not HBM: its counted VALU
     wavefront instructions (64 lanes each) per launch over the launch time,
-    against the VALU issue peak (None without a current counter summary)."""
+    against the VALU issue peak (None without a current counter summary).
+    elems_per_step: quantised elements per step (for the per-element count)."""
     valu = measured_counter(config, kernel, "valu_insts_per_launch")
     if valu is None or kernel not in prof:
         return None
@@ -832,7 +840,7 @@ def alu_roofline_of(config, prof, kernel):
     r = {"bound": "alu", "kernel": kernel, "achieved": lane_ops / avg_s, "peak": VALU_PEAK_LANE_OPS,
          "unit": "lane-op/s", "frac": lane_ops / avg_s / VALU_PEAK_LANE_OPS, "lane_ops_per_launch": lane_ops}
     if not st["work_is_flops"]:
-        r["lane_ops_per_element"] = lane_ops / (st["work"] / st["launches"] / QUANT_BYTES_PER_ELEM)
+        r["lane_ops_per_element"] = lane_ops / (elems_per_step * steps / st["launches"])
     return r
 
 
@@ -921,7 +929,8 @@ def main():
         "mfma_peak_frac": value / MXFP4_PEAK_TFLOPS,
         "roofline": roof,
         "quantize_roofline": roofline_of(config, prof, qk, args.steps) if qk else None,
-        "alu_roofline": alu_roofline_of(config, prof, qk) if qk else None,
+        "alu_roofline": alu_roofline_of(config, prof, qk, sum(L.quant_elements() for L in layers), args.steps)
+                        if qk else None,
         "kernels": kernels,
         "kernel_source_hash": kernel_source_hash(),
         "wall_s_timed": t_wall,

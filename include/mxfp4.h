@@ -161,6 +161,29 @@ int mx_quantize(const uint16_t* in, uint8_t* codes, uint8_t* scales, int64_t row
                 uint64_t seed, int mode, int transposed, void* stream);
 
 /*
+ * Both quantisations of one matrix in one pass over it: Algorithm 3 quantises
+ * dY twice, along out (dY for dX) and along the tokens (dY^T for dW).
+ *   in       [rows, cols] bf16 bits, row-major, 16-byte aligned.
+ *   codes    [rows, cols/2], scales [rows, cols/32]: in quantised along its
+ *            rows with `seed` -- mx_quantize(in, codes, scales, rows, cols, g,
+ *            seed, mode, 0, stream), byte for byte.
+ *   codes_t  [cols, rows/2], scales_t [cols, rows/32]: in^T quantised along its
+ *            rows (blocks run down the columns of `in`) with `seed_t` --
+ *            mx_quantize(in, codes_t, scales_t, cols, rows, g, seed_t, mode, 1,
+ *            stream), byte for byte.
+ *   codes and codes_t 4-byte aligned. Both rows and cols must be multiples of
+ *   the mode's block (g with the RHT, 32 without); g and mode as for
+ *   mx_quantize. The four outputs must not overlap.
+ * When the block is at most 64 and cols % 8 == 0, each workgroup quantises the
+ * tile it has read in both directions, so the input is read from memory once;
+ * otherwise both run in one launch as separate passes. Results are the same
+ * either way.
+ * Paper: Algorithm 3 (the two quantisations of dY), Algorithm 2, Sec. 3.2.
+ */
+int mx_quantize_pair(const uint16_t* in, uint8_t* codes, uint8_t* scales, uint8_t* codes_t, uint8_t* scales_t,
+                     int64_t rows, int64_t cols, int g, uint64_t seed, uint64_t seed_t, int mode, void* stream);
+
+/*
  * MXFP4 GEMM with FP32 accumulation: C[M, N] = sum_k deq(A)[m, k] * deq(B)[n, k]
  * (the MXFP4_GEMM of Algorithm 3 with groups along K; no 16/9 factor here).
  *   A_codes [M, K/2], A_scales [M, K/32]; B_codes [N, K/2], B_scales [N, K/32],

@@ -74,6 +74,8 @@ def load_library():
     lib.mx_quantize.argtypes = [vp, vp, vp, i64, i64, ci, u64, ci, ci, vp]
     lib.mx_linear_backward_mode.restype = ci
     lib.mx_linear_backward_mode.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ci, u64, ci, vp]
+    lib.mx_quantize_pair.restype = ci
+    lib.mx_quantize_pair.argtypes = [vp, vp, vp, vp, vp, i64, i64, ci, u64, u64, ci, vp]
     lib.mx_gemm_f4.restype = ci
     lib.mx_gemm_f4.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
     lib.mx_linear_backward.restype = ci
@@ -191,6 +193,23 @@ def mx_quantize(x, codes, scales, g, seed, mode, transposed=False, stream=None):
     rows, cols, p = _quant_args(x, codes, scales, bool(transposed))
     _check(load_library().mx_quantize(*p, rows, cols, g, seed & 0xFFFFFFFFFFFFFFFF, mode, 1 if transposed else 0,
                                       _stream(stream)))
+
+
+def mx_quantize_pair(x, codes, scales, codes_t, scales_t, g, seed, seed_t, mode=0, stream=None):
+    """Both quantisations of row-major bf16 x [rows, cols] in one pass: codes/scales of x
+    (blocks along cols, seed) and codes_t/scales_t of x^T [cols, rows] (blocks along rows,
+    seed_t)."""
+    rows, cols = _two_d(x, "x")
+    _arg(x, "x", "bf16", (rows, cols))
+    cs, ss = quantized_shapes(rows, cols)
+    cst, sst = quantized_shapes(cols, rows)
+    _arg(codes, "codes", "u8", cs)
+    _arg(scales, "scales", "u8", ss)
+    _arg(codes_t, "codes_t", "u8", cst)
+    _arg(scales_t, "scales_t", "u8", sst)
+    _check(load_library().mx_quantize_pair(*_ptrs(x, codes, scales, codes_t, scales_t), rows, cols, g,
+                                           seed & 0xFFFFFFFFFFFFFFFF, seed_t & 0xFFFFFFFFFFFFFFFF, mode,
+                                           _stream(stream)))
 
 
 def mx_gemm_f4(a_codes, a_scales, b_codes, b_scales, c, stream=None):

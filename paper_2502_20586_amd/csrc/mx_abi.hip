@@ -308,10 +308,19 @@ int linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, vo
       {X, q[3].codes, q[3].scales, in_features, T, seed ^ 3u, true, kt},
   };
   specs[2].colsum = colsum;
-  if (in_features > 0)
+  // For blocks of at most 64 the dY^T pass also writes Q0 (its twin: the
+  // stored dY quantised along out), so dY is read from memory once.
+  const bool twin = blk <= 64 && out_features % 8 == 0 && aligned(dY, 16);
+  if (in_features > 0 && twin) {
+    specs[2].twin_codes = q[0].codes;
+    specs[2].twin_scales = q[0].scales;
+    specs[2].twin_seed = specs[0].seed;
+    fail |= mx::launch_quant(specs + 1, 3, g, static_cast<mx::QuantMode>(mode), s);
+  } else if (in_features > 0) {
     fail |= mx::launch_quant(specs, 4, g, static_cast<mx::QuantMode>(mode), s);
-  else if (need_db)   // no GEMM to feed: only the pass that sums dY
+  } else if (need_db) {   // no GEMM to feed: only the pass that sums dY
     fail |= mx::launch_quant(&specs[2], 1, g, static_cast<mx::QuantMode>(mode), s);
+  }
   if (in_features > 0) fail |= mx::launch_gemm(gp, 2, partial, s);
   if (need_db) fail |= mx::colsum_reduce(colsum, db, out_features, nblk, accumulate, s);
   return fail ? MX_ERR_HIP : MX_OK;
@@ -359,6 +368,28 @@ int mx_rht_sr_quantize(const uint16_t* in, uint8_t* codes, uint8_t* scales, int6
 int mx_rht_sr_quantize_t(const uint16_t* in_t, uint8_t* codes, uint8_t* scales, int64_t rows,
                          int64_t cols, int g, uint64_t seed, void* stream) {
   return mx_quantize(in_t, codes, scales, rows, cols, g, seed, MX_MODE_RHT_SR, 1, stream);
+}
+
+int mx_quantize_pair(const uint16_t* in, uint8_t* codes, uint8_t* scales, uint8_t* codes_t, uint8_t* scales_t,
+                     int64_t rows, int64_t cols, int g, uint64_t seed, uint64_t seed_t, int mode, void* stream) {
+  int st = validate_quant(in, codes, scales, rows, cols, g, false, mode);
+  if (st != MX_OK) return st;
+  if ((st = validate_quant(in, codes_t, scales_t, cols, rows, g, true, mode)) != MX_OK) return st;
+  if (rows == 0 || cols == 0) return MX_OK;
+  if (!aligned(in, 16)) return MX_ERR_ALIGN;
+  if ((st = check_device()) != MX_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = check_not_capturing(s)) != MX_OK) return st;
+  const mx::QuantMode m = static_cast<mx::QuantMode>(mode);
+  mx::QuantSpec spec_t{in, codes_t, scales_t, cols, rows, seed_t, true, false};
+  if (mode_block(mode, g) <= 64 && cols % 8 == 0) {
+    spec_t.twin_codes = codes;
+    spec_t.twin_scales = scales;
+    spec_t.twin_seed = seed;
+    return mx::launch_quant(&spec_t, 1, g, m, s) ? MX_ERR_HIP : MX_OK;
+  }
+  const mx::QuantSpec specs[2] = {spec_t, {in, codes, scales, rows, cols, seed, false, false}};
+  return mx::launch_quant(specs, 2, g, m, s) ? MX_ERR_HIP : MX_OK;
 }
 
 int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B_codes,

@@ -32,6 +32,13 @@ struct QuantSpec {
   bool transposed;
   bool ktiled;
   float* colsum = nullptr;
+  // transposed only, optional (g <= 64, rows % 8 == 0, `in` 16-byte aligned):
+  // also quantise the stored matrix itself -- [cols, rows], blocks along rows
+  // -- with twin_seed into twin_codes / twin_scales (same layout kind), in the
+  // same pass over the input.
+  uint8_t* twin_codes = nullptr;
+  uint8_t* twin_scales = nullptr;
+  uint64_t twin_seed = 0;
 };
 
 // The paper's quantiser, its ablations (Table 2 rows) and the cheaper-noise

@@ -280,6 +280,12 @@ struct QuantJob {
   int codes16;   // codes 16-byte aligned (16-byte stores of staged transposed output)
   int wg_begin, wg_end;
   float* colsum; // transposed, optional: [cols / g][rows] sums of the input per g-block
+  // transposed, optional: the twin, the stored matrix itself ([cols, rows],
+  // blocks along rows) quantised in the same pass with its own seed, into
+  // tcodes / tscales in the same output layout.
+  uint8_t* tcodes;
+  uint8_t* tscales;
+  uint64_t tseed;
 };
 
 struct QuantJobs {
@@ -435,7 +441,17 @@ struct ColsCfg {
 // (bf16, before the sign flip) over each g-block, in FP32: every lane sums its
 // g/4 values of a row in chunk-then-element order, the quad adds the four lane
 // sums as (q0 + q1) + (q2 + q3), and lane q stores row RPQ k + q's sum.
-template <int G, bool RHT, int NB, bool KT, int RPQ, bool LW2, bool CS = false>
+//
+// TW: the job also quantises its twin (see QuantJob) -- the same input, stored
+// [cols, rows], along its stored rows. After writing a tile out, the workgroup
+// quantises the twin's blocks that lie in the tile it has just read (its
+// g-block group's stored rows and its TR stored columns), from the cache: the
+// input is read from memory once for both outputs. Each quad takes blocks
+// b = quad, quad + 64, ... of the tile's (stored row, column block) pairs and
+// runs the row-major path's arithmetic on them, so the twin's codes and scales
+// are exactly those of a row-major job on the stored matrix. Needs TR % G == 0
+// (RPQ = 4, g <= 64) and stored rows whose length is a multiple of 8.
+template <int G, bool RHT, int NB, bool KT, int RPQ, bool LW2, bool CS = false, bool TW = false>
 __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64_t nwg, uint8_t* smem) {
   using CC = ColsCfg<G>;
   constexpr int NC = G / 32;
@@ -461,6 +477,18 @@ __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64
     for (int r = 0; r < NC; ++r)
 #pragma unroll
       for (int e = 0; e < 8; ++e) smask[r][e] = sign_mask_col<G, RHT>(sbits, flip, r, e);
+  }
+  // The twin: its row-major sign masks and seed, and a job view of its output
+  // (the stored matrix, [cols, rows]).
+  const uint32_t tseed_lo = (uint32_t)job.tseed, tseed_hi = (uint32_t)(job.tseed >> 32);
+  uint32_t tmask[TW ? NC : 1][4];
+  QuantJob twin{};
+  if constexpr (TW) {
+    sign_masks_pairs<G, RHT>(tseed_hi, q, tmask);
+    twin.codes = job.tcodes;
+    twin.scales = job.tscales;
+    twin.rows = job.cols;
+    twin.cols = job.rows;
   }
   const int64_t rows = job.rows, cols = job.cols;
   const int64_t rtiles = (rows + TR - 1) / TR;
@@ -666,6 +694,44 @@ __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64
         job.scales[(row * cols + kcol0) / 32 + bi] = scales_lds[lr * CC::kScaleRow + bi];
       }
     }
+    if constexpr (TW) {
+      static_assert(TR % G == 0, "twin blocks must not straddle row tiles");
+      constexpr int kBpt = TR / G;                      // twin blocks per stored row of the tile
+      const int64_t srow0 = kcol0;                      // first stored row of the tile
+      const int64_t nblk = min(nk * G, cols - srow0) * kBpt;
+      for (int64_t b = tid >> 2; b < nblk; b += kThreads / 4) {
+        const int64_t srow = srow0 + b / kBpt;
+        const int64_t scol = row0 + (b % kBpt) * G;     // first stored column of the block
+        if (scol >= rows) continue;                     // rows % G == 0: a block is whole or absent
+        const uint16_t* src = job.in + srow * rows + scol + q * 8;
+        uint4 raw2[NC];
+#pragma unroll
+        for (int r = 0; r < NC; ++r) raw2[r] = *reinterpret_cast<const uint4*>(src + r * 32);
+        float v2[NC][8];
+#pragma unroll
+        for (int r = 0; r < NC; ++r) {
+          const uint32_t w[4] = {raw2[r].x ^ tmask[r][0], raw2[r].y ^ tmask[r][1], raw2[r].z ^ tmask[r][2],
+                                 raw2[r].w ^ tmask[r][3]};
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            v2[r][2 * d] = __uint_as_float(w[d] << 16);
+            v2[r][2 * d + 1] = __uint_as_float(w[d] & 0xFFFF0000u);
+          }
+        }
+        if (RHT) butterfly<G>(v2, q);
+        const uint64_t chunk0 = (uint64_t)(srow * rows + scol + q * 8) >> 3;
+        Rand4 rnd8{};
+#pragma unroll
+        for (int r = 0; r < NC; ++r) {
+          if (NB == 8 && (r & 1) == 0)
+            rnd8 = philox4x32_10((uint32_t)(chunk0 + 4 * r), (uint32_t)((chunk0 + 4 * r) >> 32), 0, 0, tseed_lo,
+                                 tseed_hi);
+          uint32_t sbyte;
+          const uint32_t packed = quantise_chunk<NB>(v2[r], chunk0 + 4 * r, tseed_lo, tseed_hi, &sbyte, rnd8, r & 1);
+          store_chunk<KT>(twin, srow, scol + q * 8 + r * 32, packed, sbyte, q == (r & 3));
+        }
+      }
+    }
     rt = rt2;
     kg = kg2;
   }
@@ -675,7 +741,10 @@ __device__ __forceinline__ void cols_body(const QuantJob& job, int64_t wg, int64
 // so that the extra registers of that path do not cost the others occupancy).
 // g <= 64 fits 128 VGPRs: four waves per SIMD to hide the loads' latency
 // behind the VALU work of the others.
-template <int G, bool RHT, int NB, bool KT, bool CS>
+// TW likewise for a launch that holds a job with a twin (g <= 64, at
+// load_rows == 4; at most one such job per launch in practice, the dY^T of a
+// backward pass, which may also sum its input).
+template <int G, bool RHT, int NB, bool KT, bool CS, bool TW>
 __global__ __launch_bounds__(kThreads, G <= 64 ? 4 : 1) void quant_kernel(QuantJobs jobs) {
   extern __shared__ __align__(16) uint8_t smem[];
   int j = 0;
@@ -687,6 +756,10 @@ __global__ __launch_bounds__(kThreads, G <= 64 ? 4 : 1) void quant_kernel(QuantJ
   const int64_t nwg = job.wg_end - job.wg_begin;
   if (!job.transposed)
     rows_body<G, RHT, NB, KT>(job, wg, nwg);
+  else if (TW && job.tcodes && job.colsum)
+    cols_body<G, RHT, NB, KT, 4, true, true, TW>(job, wg, nwg, smem);
+  else if (TW && job.tcodes)
+    cols_body<G, RHT, NB, KT, 4, true, false, TW>(job, wg, nwg, smem);
   else if (CS && job.colsum)   // launch_jobs_g admits colsum jobs only at load_rows == kRpqMax
     cols_body<G, RHT, NB, KT, ColsCfg<G>::kRpqMax, true, CS>(job, wg, nwg, smem);
   else if (job.load_rows == 4)
@@ -716,6 +789,11 @@ int launch_jobs_g(QuantJobs jobs, hipStream_t stream) {
     // Four rows per quad only where the registers allow it (g <= 64).
     if (G > 64 && jb.load_rows == 4) jb.load_rows = 2;
     if (jb.colsum && jb.load_rows != ColsCfg<G>::kRpqMax) return -1;
+    // A twin needs four rows per quad (g <= 64) and 16-byte loads along the
+    // stored rows (rows % 8 == 0, 16-byte aligned input).
+    if (jb.tcodes && (G > 64 || !jb.transposed || jb.load_rows != 4 || jb.rows % 8 != 0 || jb.rows % G != 0 ||
+                      reinterpret_cast<uintptr_t>(jb.in) % 16 != 0))
+      return -1;
     int64_t need;
     if (!jb.transposed) {
       const int64_t nblocks = jb.rows * (jb.cols / G);
@@ -730,20 +808,34 @@ int launch_jobs_g(QuantJobs jobs, hipStream_t stream) {
     jb.wg_end = wg;
   }
   if (wg == 0) return 0;
+  // Algorithmic bytes: a twin adds its codes and scales, not another read.
   double bytes = 0;
-  for (int i = 0; i < jobs.count; ++i) bytes += (double)jobs.j[i].rows * jobs.j[i].cols * (2.0 + 0.5 + 1.0 / 32);
+  for (int i = 0; i < jobs.count; ++i)
+    bytes += (double)jobs.j[i].rows * jobs.j[i].cols * (2.0 + (jobs.j[i].tcodes ? 2.0 : 1.0) * (0.5 + 1.0 / 32));
   TraceScope trace(quant_name<G, RHT, NB>(), bytes, false);
   bool any_t = false;
   for (int i = 0; i < jobs.count; ++i) any_t = any_t || jobs.j[i].transposed;
-  bool any_cs = false;
+  bool any_cs = false, any_tw = false;
   for (int i = 0; i < jobs.count; ++i) any_cs = any_cs || jobs.j[i].colsum != nullptr;
+  for (int i = 0; i < jobs.count; ++i) any_tw = any_tw || jobs.j[i].tcodes != nullptr;
   const int lds = any_t ? ColsCfg<G>::kLds : 0;
+  if constexpr (G <= 64) {
+    if (any_tw) {
+      if (any_cs)
+        hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, true, true>), dim3((unsigned)wg), dim3(kThreads), lds,
+                              stream, trace.start(), trace.stop(), 0, jobs);
+      else
+        hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, false, true>), dim3((unsigned)wg), dim3(kThreads), lds,
+                              stream, trace.start(), trace.stop(), 0, jobs);
+      return hipGetLastError() == hipSuccess ? 0 : -1;
+    }
+  }
   if (any_cs)
-    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, true>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
-                          trace.start(), trace.stop(), 0, jobs);
+    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, true, false>), dim3((unsigned)wg), dim3(kThreads), lds,
+                          stream, trace.start(), trace.stop(), 0, jobs);
   else
-    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, false>), dim3((unsigned)wg), dim3(kThreads), lds, stream,
-                          trace.start(), trace.stop(), 0, jobs);
+    hipExtLaunchKernelGGL((quant_kernel<G, RHT, NB, KT, false, false>), dim3((unsigned)wg), dim3(kThreads), lds,
+                          stream, trace.start(), trace.stop(), 0, jobs);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -809,6 +901,12 @@ int launch_quant(const QuantSpec* specs, int count, int g, QuantMode mode, hipSt
     j.transposed = specs[i].transposed ? 1 : 0;
     j.colsum = specs[i].colsum;
     if (j.colsum && !j.transposed) return -1;
+    j.tcodes = specs[i].twin_codes;
+    j.tscales = specs[i].twin_scales;
+    j.tseed = specs[i].twin_seed;
+    if ((j.tcodes == nullptr) != (j.tscales == nullptr)) return -1;
+    // The twin's K-tiled offsets are 32-bit too; its blocks run along `rows`.
+    if (j.tcodes && kt && (j.rows % 128 != 0 || j.rows * j.cols / 2 >= (int64_t(1) << 31))) return -1;
     const uintptr_t addr = reinterpret_cast<uintptr_t>(j.in);
     j.load_rows = (j.rows % 4 == 0 && addr % 8 == 0) ? 4 : (j.rows % 2 == 0 && addr % 4 == 0) ? 2 : 1;
     j.codes16 = reinterpret_cast<uintptr_t>(j.codes) % 16 == 0 ? 1 : 0;

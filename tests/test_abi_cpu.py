@@ -88,6 +88,26 @@ def test_quantize_modes_validation():
         assert q(None, FAKE, FAKE, 4, 96, 48, 0, mode, 1, None) == -1
 
 
+def test_quantize_pair_validation():
+    """mx_quantize_pair: both directions' block rule (rows and cols multiples of the
+    block), every output pointer and the 16-byte input alignment are checked first."""
+    lib = _lib()
+    f = lib.mx_quantize_pair
+    RHT_SR, SR = binding.MX_MODE_RHT_SR, binding.MX_MODE_SR
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 64, 128, 48, 0, 2, RHT_SR, None) == -2     # bad g
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 96, 128, 64, 0, 2, RHT_SR, None) == -3     # rows % g
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 128, 96, 64, 0, 2, RHT_SR, None) == -3     # cols % g
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 2, 9, None) == -8           # bad mode
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 48, 64, 64, 0, 2, SR, None) == -3          # rows % 32
+    for i in range(5):                                                                # each pointer
+        args = [FAKE] * 5
+        args[i] = None
+        assert f(*args, 64, 128, 64, 0, 2, RHT_SR, None) == -1
+    assert f(FAKE + 8, FAKE, FAKE, FAKE, FAKE, 64, 128, 64, 0, 2, RHT_SR, None) == -4  # in 16-byte aligned
+    assert f(FAKE, FAKE, FAKE, FAKE + 2, FAKE, 64, 128, 64, 0, 2, RHT_SR, None) == -4
+    assert f(None, None, None, None, None, 0, 128, 64, 0, 2, RHT_SR, None) == 0       # empty
+
+
 def test_linear_backward_modes_validation():
     lib = _lib()
     f = lib.mx_linear_backward_mode

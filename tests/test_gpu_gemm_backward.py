@@ -257,7 +257,9 @@ def test_kernel_tracing_counts_launches_and_work():
     quant = [v for k, v in stats.items() if k.startswith("quant")]
     gemm = [v for k, v in stats.items() if k.startswith("gemm")]
     assert len(quant) == 1 and quant[0]["launches"] == 3 and not quant[0]["work_is_flops"]
-    assert quant[0]["work"] == 3 * (2 * t * fout + fin * fout + fin * t) * (2 + 0.5 + 1 / 32)
+    # Algorithmic bytes: each operand's codes and scales, and each input read
+    # once (dY serves Q0 and Q2 in one pass at g = 64).
+    assert quant[0]["work"] == 3 * ((t * fout + fin * fout + fin * t) * 2 + (2 * t * fout + fin * fout + fin * t) * (0.5 + 1 / 32))
     assert len(gemm) == 1 and gemm[0]["launches"] == 3 and gemm[0]["work_is_flops"]
     assert gemm[0]["work"] == 3 * 4 * t * fin * fout
     assert all(v["total_ms"] > 0 for v in stats.values())
