@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libmxfp4.so")
-SOURCES = ["mx_quant.hip", "mx_gemm.hip", "mx_abi.hip", "mx_profile.hip"]
+SOURCES = ["mx_quant_rht_sr.hip", "mx_quant_sr8.hip", "mx_quant_ablation.hip", "mx_quant.hip", "mx_gemm.hip",
+           "mx_abi.hip", "mx_profile.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops off: no v_pk_*_f32 from the compiler. Denormals kept and no
