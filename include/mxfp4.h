@@ -196,10 +196,25 @@ int mx_quantize_pair(const uint16_t* in, uint8_t* codes, uint8_t* scales, uint8_
  * per-stream workspace (as for mx_linear_backward), into the K-tiled layout
  * the GEMM kernels load fastest: about 0.53 byte of scratch per element of A
  * and of B. When few output tiles meet a long K, K is split and FP32 partial
- * sums go through the same workspace.
+ * sums go through the same workspace. mx_gemm_f4_workspace_bytes gives the
+ * total.
  */
 int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B_codes,
                const uint8_t* B_scales, float* C, int64_t M, int64_t N, int64_t K, void* stream);
+
+/* Bytes of workspace mx_gemm_f4 needs for these sizes (0 for invalid or empty
+ * sizes, or when it needs none). */
+int64_t mx_gemm_f4_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * Frees the workspace the library keeps for the current device and `stream`
+ * (see mx_linear_backward), in stream order: the block is released after the
+ * work already enqueued on `stream`, so calls enqueued before stay valid. The
+ * next call on that stream allocates a new one. MX_OK also when the stream has
+ * none; MX_ERR_HIP if the free fails. Not for a stream that is being captured
+ * (MX_ERR_CAPTURE).
+ */
+int mx_release_workspace(void* stream);
 
 /*
  * Algorithm 3: MXFP4 backward pass of a linear layer y = x W^T (no bias).
@@ -222,8 +237,9 @@ int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B
  * stream. A call that needs more than the workspace holds grows it in stream
  * order (the old block is freed after the work already enqueued on `stream`,
  * the new one allocated from a pool the library owns); the workspace is held
- * until the process ends. Because a call may allocate, it refuses a stream
- * that is being captured into a graph (MX_ERR_CAPTURE).
+ * until mx_release_workspace or the end of the process. Because a call may
+ * allocate, it refuses a stream that is being captured into a graph
+ * (MX_ERR_CAPTURE).
  */
 int mx_linear_backward(const uint16_t* dY, const uint16_t* X, const uint16_t* W, float* dX,
                        float* dW, int64_t T, int64_t in_features, int64_t out_features, int g,

@@ -76,6 +76,10 @@ def load_library():
     lib.mx_linear_backward_mode.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ci, u64, ci, vp]
     lib.mx_quantize_pair.restype = ci
     lib.mx_quantize_pair.argtypes = [vp, vp, vp, vp, vp, i64, i64, ci, u64, u64, ci, vp]
+    lib.mx_gemm_f4_workspace_bytes.restype = i64
+    lib.mx_gemm_f4_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.mx_release_workspace.restype = ci
+    lib.mx_release_workspace.argtypes = [vp]
     lib.mx_gemm_f4.restype = ci
     lib.mx_gemm_f4.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
     lib.mx_linear_backward.restype = ci
@@ -223,6 +227,16 @@ def mx_gemm_f4(a_codes, a_scales, b_codes, b_scales, c, stream=None):
     _arg(b_scales, "b_scales", "u8", (n, k // 32))
     _arg(c, "c", "f32", (m, n))
     _check(load_library().mx_gemm_f4(*_ptrs(a_codes, a_scales, b_codes, b_scales, c), m, n, k, _stream(stream)))
+
+
+def mx_gemm_f4_workspace_bytes(m, n, k):
+    """Bytes of workspace mx_gemm_f4 needs for an [m, k] x [n, k] product."""
+    return int(load_library().mx_gemm_f4_workspace_bytes(m, n, k))
+
+
+def mx_release_workspace(stream=None):
+    """Free the library's workspace for the current device and stream, in stream order."""
+    _check(load_library().mx_release_workspace(_stream(stream)))
 
 
 def _backward_args(dy, x, w, dx, dw, db=None, dx_kind="f32"):

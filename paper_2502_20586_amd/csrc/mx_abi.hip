@@ -392,6 +392,60 @@ int mx_quantize_pair(const uint16_t* in, uint8_t* codes, uint8_t* scales, uint8_
   return mx::launch_quant(specs, 2, g, m, s) ? MX_ERR_HIP : MX_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Workspace of mx_gemm_f4: split-K partial sums first, then (K-tiled
+// kernels) the K-tiled copies of A's codes and scales and B's codes and
+// scales at off[0..3]. Returns the total bytes.
+int64_t gemm_f4_layout(const mx::GemmArgs& g, bool* kt, int64_t* partial_bytes, int64_t off[4]) {
+  *kt = g.K > 0 && mx::gemm_takes_ktiled(&g, 1);
+  *partial_bytes = round_up(mx::gemm_workspace_bytes(&g, 1), 256);
+  int64_t bytes = *partial_bytes;
+  for (int i = 0; i < 4; ++i) off[i] = 0;
+  if (*kt) {
+    const int64_t parts[4] = {g.M * g.K / 2, g.M * g.K / 32, g.N * g.K / 2, g.N * g.K / 32};
+    for (int i = 0; i < 4; ++i) {
+      off[i] = bytes;
+      bytes = round_up(bytes + parts[i], 256);
+    }
+  }
+  return bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t mx_gemm_f4_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K < 0 || K % 32 != 0 || N >= mx::kGemmMaxN) return 0;
+  const mx::GemmArgs g{nullptr, nullptr, nullptr, nullptr, nullptr, M, N, K, 1.0f, false};
+  bool kt;
+  int64_t partial_bytes, off[4];
+  return gemm_f4_layout(g, &kt, &partial_bytes, off);
+}
+
+int mx_release_workspace(void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  int st = check_not_capturing(s);
+  if (st != MX_OK) return st;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MX_ERR_HIP;
+  Workspace* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    auto it = g_workspaces.find({dev, s});
+    if (it == g_workspaces.end()) return MX_OK;
+    ws = it->second.get();
+  }
+  std::lock_guard<std::mutex> lock(ws->mu);
+  if (ws->ptr && hipFreeAsync(ws->ptr, s) != hipSuccess) return MX_ERR_HIP;
+  ws->ptr = nullptr;
+  ws->bytes = 0;
+  return MX_OK;
+}
+
 int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B_codes,
                const uint8_t* B_scales, float* C, int64_t M, int64_t N, int64_t K, void* stream) {
   if (M < 0 || N < 0 || K < 0 || K % 32 != 0 || N >= mx::kGemmMaxN) return MX_ERR_SHAPE;
@@ -409,16 +463,9 @@ int mx_gemm_f4(const uint8_t* A_codes, const uint8_t* A_scales, const uint8_t* B
   // contiguous range; row-major scale loads touch one cache line per row):
   // a memory-bound pass of about 1.06 bytes per operand element, small next
   // to the GEMM it speeds up.
-  const bool kt = K > 0 && mx::gemm_takes_ktiled(&g, 1);
-  const int64_t partial_bytes = round_up(mx::gemm_workspace_bytes(&g, 1), 256);
-  int64_t bytes = partial_bytes, off[4] = {0, 0, 0, 0};
-  if (kt) {
-    const int64_t parts[4] = {M * K / 2, M * K / 32, N * K / 2, N * K / 32};
-    for (int i = 0; i < 4; ++i) {
-      off[i] = bytes;
-      bytes = round_up(bytes + parts[i], 256);
-    }
-  }
+  bool kt;
+  int64_t partial_bytes, off[4];
+  const int64_t bytes = gemm_f4_layout(g, &kt, &partial_bytes, off);
   void* ws = nullptr;
   WorkspaceLease lease;
   if ((st = lease.acquire(bytes, s, &ws)) != MX_OK) return st;

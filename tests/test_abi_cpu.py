@@ -108,6 +108,25 @@ def test_quantize_pair_validation():
     assert f(None, None, None, None, None, 0, 128, 64, 0, 2, RHT_SR, None) == 0       # empty
 
 
+def test_gemm_workspace_bytes():
+    """mx_gemm_f4_workspace_bytes: 0 for invalid or empty sizes; for K % 128 == 0 at
+    least the K-tiled copies of both operands (0.53125 byte per element, each part
+    rounded up to 256 bytes); split-K partial sums on top when few tiles meet a long K."""
+    lib = _lib()
+    f = lib.mx_gemm_f4_workspace_bytes
+    assert f(0, 64, 128) == 0 and f(64, 0, 128) == 0 and f(64, 64, 96 + 1) == 0 and f(-1, 64, 128) == 0
+    assert f(64, 1 << 24, 128) == 0                                          # N limit
+    up = lambda v: (v + 255) // 256 * 256
+    for m, n, k in ((4096, 4096, 4096), (16384, 4096, 12288), (256, 384, 1024)):
+        copies = up(m * k // 2) + up(m * k // 32) + up(n * k // 2) + up(n * k // 32)
+        got = f(m, n, k)
+        assert got >= copies, (m, n, k)
+        assert got - copies in (0,) or (got - copies) % (m * n * 4) == 0, (m, n, k, got - copies)
+    assert f(8192, 8192, 8192) == up(8192 * 4096) * 2 + up(8192 * 256) * 2   # many tiles: no split
+    assert f(256, 256, 65536) > up(256 * 32768) * 2 + up(256 * 2048) * 2    # one tile, long K: split
+    assert f(64, 64, 96) == 0                                                # K % 128 != 0: no copies
+
+
 def test_linear_backward_modes_validation():
     lib = _lib()
     f = lib.mx_linear_backward_mode

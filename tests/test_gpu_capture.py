@@ -53,7 +53,10 @@ def test_entry_points_refuse_a_capturing_stream():
         "mx_rht_sr_quantize": lambda s: mx.mx_rht_sr_quantize(ddy, codes, scales, g, seed, stream=s),
         "mx_rht_sr_quantize_t": lambda s: mx.mx_rht_sr_quantize_t(ddy, codes_t, scales_t, g, seed, stream=s),
         "mx_quantize": lambda s: mx.mx_quantize(ddy, codes, scales, g, seed, mx.MX_MODE_NR, stream=s),
+        "mx_quantize_pair": lambda s: mx.mx_quantize_pair(ddy, codes, scales, codes_t, scales_t, g, seed,
+                                                          seed ^ 2, stream=s),
         "mx_gemm_f4": lambda s: mx.mx_gemm_f4(codes, scales, codes, scales, c, stream=s),
+        "mx_release_workspace": lambda s: mx.mx_release_workspace(stream=s),
         "mx_linear_backward": lambda s: mx.mx_linear_backward(ddy, dx_in, dw_in, dx, dw, g, seed, stream=s),
         "mx_linear_backward_mode": lambda s: mx.mx_linear_backward_mode(ddy, dx_in, dw_in, dx, dw, g, seed,
                                                                         mx.MX_MODE_SR, stream=s),
@@ -87,6 +90,7 @@ def test_entry_points_refuse_a_capturing_stream():
     for tns in (dx, dw, db, c):
         assert torch.all(tns == 7.0)
     assert torch.all(codes == 0) and torch.all(scales == 0)
+    assert torch.all(codes_t == 0) and torch.all(scales_t == 0)
 
     note("capture: the stream works normally afterwards")
     mx.mx_linear_backward(ddy, dx_in, dw_in, dx, dw, g, seed, stream=s)

@@ -117,6 +117,36 @@ def test_split_k_gemm_is_deterministic():
     assert rel_err(g1, oracle.gemm_f64(*a, *b)) <= TOL
 
 
+def test_release_workspace_between_gemms():
+    """mx_release_workspace frees the stream's workspace in stream order: a GEMM
+    enqueued before the release, one after it (which allocates again, here a
+    split-K problem whose workspace also holds partial sums) and the release of
+    a stream that holds none all give the oracle's results."""
+    torch = torch_gpu()
+    import paper_2502_20586_amd as mx
+    rng = np.random.default_rng(11)
+    a, b = _rand_mx(rng, 256, 8192), _rand_mx(rng, 384, 8192)
+    assert mx.mx_gemm_f4_workspace_bytes(256, 384, 8192) > 256 * 8192 * 0.53
+    ops = [to_dev_u8(pack_codes(a[0])), to_dev_u8(a[1]), to_dev_u8(pack_codes(b[0])), to_dev_u8(b[1])]
+    ref = oracle.gemm_f64(*a, *b)
+    s = torch.cuda.Stream()
+    outs = [torch.full((256, 384), float("nan"), device="cuda") for _ in range(2)]
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        mx.mx_gemm_f4(*ops, outs[0])
+        mx.mx_release_workspace()
+        mx.mx_release_workspace()                 # none left: still MX_OK
+        mx.mx_gemm_f4(*ops, outs[1])
+    torch.cuda.current_stream().wait_stream(s)
+    s.synchronize()
+    mx.mx_release_workspace(s)
+    got = [host(c) for c in outs]
+    assert np.array_equal(got[0], got[1])
+    assert rel_err(got[0], ref) <= TOL
+    fresh = torch.cuda.Stream()
+    mx.mx_release_workspace(fresh)                # a stream the library never saw
+
+
 def test_gemm_k_zero_and_empty():
     torch = torch_gpu()
     import paper_2502_20586_amd as mx
