@@ -122,6 +122,8 @@ def parse():
     ap.add_argument("--rht-variance", action="store_true",
                     help="variance of the SR inner-product estimator with and without the RHT (the figure of "
                          "Sec. 3.2) and the flush-to-zero statistic, through the HIP path")
+    ap.add_argument("--co-schedule", action="store_true",
+                    help="two independent GPT-6.7B block backwards on one stream and on two streams")
     ap.add_argument("--configs", action="store_true",
                     help="instead of the step: GPT-1.3B (every g) and GPT-6.7B block backward end to end, "
                          "with BF16 / FP8 GEMM baselines on the same shapes")
@@ -420,6 +422,60 @@ def rht_variance(torch, mx, draws=64, oracle_rows=256):
         flush[name + "_oracle_first_256_rows"] = float(pz[mask].sum() / mask.sum())
     print(f"[var] flush to zero: {flush}", file=sys.stderr, flush=True)
     return {"variance": rows, "flush_to_zero": flush}
+
+
+def co_schedule(torch, mx, reps=10, rounds=3):
+    """Two independent GPT-6.7B block backwards (two micro-batches' worth of
+    inputs and outputs), run back to back on one stream and concurrently on two
+    streams of the same priority, the second stream taking the linears in
+    reverse order so that its quantiser launches tend to meet the first
+    stream's GEMM launches. A GEMM workgroup holds a whole SIMD's registers (one
+    wave per SIMD), so the two kernels cannot share a CU: any gain comes from
+    the hardware filling CUs that one launch leaves idle (launch tails, the
+    tiles' synchronised store bursts) with the other stream's work."""
+    _, layers = load_layers(torch, "gpt6.7b")
+    g = 64
+    other = []
+    for L in layers:
+        c = Layer.__new__(Layer)
+        c.__dict__.update(L.__dict__)
+        c.dy, c.x, c.w = L.dy.clone(), L.x.clone(), L.w.clone()
+        c.dx, c.dw = torch.empty_like(L.dx), torch.empty_like(L.dw)
+        other.append(c)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def run(seq_a, seq_b, n):
+        cur = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        sa.wait_stream(cur)
+        sb.wait_stream(cur)
+        for _ in range(n):
+            for s, seq in ((sa, seq_a), (sb, seq_b)):
+                for L in seq:
+                    mx.mx_linear_backward(L.dy, L.x, L.w, L.dx, L.dw, g, SEED, stream=s)
+        cur.wait_stream(sa)
+        cur.wait_stream(sb)
+        e1.record(cur)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    cases = {"one_stream": (layers + other, []), "two_streams_same_order": (layers, other),
+             "two_streams_reversed": (layers, other[::-1])}
+    for a, b in cases.values():
+        run(a, b, 3)
+    times = {k: [] for k in cases}
+    for _ in range(rounds):
+        for k, (a, b) in cases.items():
+            times[k].append(run(a, b, reps))
+    med = {k: sorted(v)[len(v) // 2] for k, v in times.items()}
+    for s in (sa, sb):
+        mx.mx_release_workspace(s)
+    return {"workload": "two gpt6.7b block backwards (T=16384, hidden 4096, g=64), independent inputs",
+            "ms_per_two_blocks": {k: round(v, 4) for k, v in med.items()},
+            "all_rounds_ms": {k: [round(t, 4) for t in v] for k, v in times.items()},
+            "gain_vs_one_stream": {k: round(med["one_stream"] / v - 1, 4) for k, v in med.items()
+                                   if k != "one_stream"}}
 
 
 def gemm_baselines(torch, layers, reps=10):
@@ -873,6 +929,9 @@ def main():
         return
     if args.rht_variance:
         print(json.dumps({"rht_variance": rht_variance(torch, mx)}))
+        return
+    if args.co_schedule:
+        print(json.dumps({"co_schedule": co_schedule(torch, mx)}))
         return
     config = args.config
     t0 = time.perf_counter()
