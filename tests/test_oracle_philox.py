@@ -124,6 +124,31 @@ def test_noise_stream_equals_pytorch_engine_sequence():
     assert np.array_equal(halves.reshape(rows, cols), r16.astype(np.uint64))
 
 
+@pytest.mark.skipif(shutil.which("g++") is None or _torch_header() is None,
+                    reason="needs g++ and PyTorch's C++ headers")
+def test_sign_vector_bits_from_pytorch_engine():
+    """Every position of S, bit by bit, from the independent engine: S_j = -1
+    iff bit j % 32 of output word (j / 32) % 4 of the engine at offset j / 128,
+    subsequence 2^32, seeded with hi32(seed) << 32 (the layout the library's
+    header documents). A swapped word, a shifted bit or a counter in the wrong
+    slot fails here even though it would stay balanced."""
+    seeds = [0xABCDEF0100000000, 0x00000001DEADBEEF, 0xFFFFFFFF00000000, 0x8000000000000007]
+    with tempfile.TemporaryDirectory() as d:
+        src = os.path.join(d, "p.cpp")
+        exe = os.path.join(d, "p")
+        open(src, "w").write(TORCH_PROBE)
+        subprocess.run(["g++", "-O1", "-std=c++17", "-I" + _torch_header(), src, "-o", exe],
+                       check=True, capture_output=True)
+        lines = [f"{(s >> 32) << 32} {1 << 32} {off}" for s in seeds for off in (0, 1)]
+        out = subprocess.run([exe], input="\n".join(lines) + "\n", capture_output=True, text=True,
+                             check=True).stdout.split("\n")
+    for i, s in enumerate(seeds):
+        words = [int(v) for line in out[2 * i:2 * i + 2] for v in line.split()]   # 8 words: offsets 0, 1
+        expect = np.array([-1.0 if (words[j // 32] >> (j % 32)) & 1 else 1.0 for j in range(256)])
+        for g in (32, 64, 128, 256):
+            assert np.array_equal(sign_vector(s, g), expect[:g]), (hex(s), g)
+
+
 def test_sign_vector_depends_only_on_high_word_and_is_balanced():
     for g in (32, 64, 128, 256):
         s = sign_vector(0xABCDEF0100000000, g)
