@@ -41,7 +41,8 @@ int check_device() {
 // pool the library owns. A lease holds the workspace's lock from the moment
 // its address is handed out until the work that uses it has been enqueued,
 // so a concurrent call on the same stream cannot free it in between.
-// Workspaces are held until the process ends.
+// A workspace is held until mx_release_workspace frees it (in stream order)
+// or the process ends.
 std::mutex g_pool_mutex;
 hipMemPool_t g_pools[kMaxDevices];
 bool g_pool_tried[kMaxDevices];

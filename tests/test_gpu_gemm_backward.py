@@ -329,7 +329,7 @@ def test_linear_backward_gpt1p3b_blocks(g):
     _check_backward_blocks(dy, x, w, g, seed, dx, dw, np.random.default_rng(g))
 
 
-@pytest.mark.parametrize("name", ["qkv", "proj"])
+@pytest.mark.parametrize("name", ["qkv", "proj", "fc1", "fc2"])
 def test_linear_backward_gpt6p7b_blocks(name):
     """GPT-6.7B linears at full size (T = 16384, hidden 4096, dY with 0.5% of
     blocks x1000); sampled blocks of dX and dW checked against the oracle."""
