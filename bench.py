@@ -522,7 +522,18 @@ def gemm_baselines(torch, layers, reps=10):
         ms = timed(fp8)
         cast_ms = timed(cast)
         out["fp8_e4m3"] = {"ms_per_step": ms, "tflops": flops / (ms * 1e-3) / 1e12,
-                           "note": "GEMMs only; operands cast to E4M3 beforehand"}
+                           "note": "GEMMs only; operands cast to E4M3 beforehand; bf16 outputs"}
+
+        def fp8_f32():
+            for a, b, at, x in pre:
+                torch._scaled_mm(a, b, scale_a=one, scale_b=one, out_dtype=torch.float32)
+                torch._scaled_mm(at, x, scale_a=one, scale_b=one, out_dtype=torch.float32)
+        try:
+            ms32 = timed(fp8_f32)
+            out["fp8_e4m3_f32_out"] = {"ms_per_step": ms32, "tflops": flops / (ms32 * 1e-3) / 1e12,
+                                       "note": "GEMMs only, FP32 dX and dW as the MXFP4 step writes them"}
+        except Exception as e:  # report, do not hide
+            out["fp8_e4m3_f32_out"] = {"error": repr(e)[:200]}
         out["fp8_e4m3_with_cast"] = {
             "ms_per_step": ms + cast_ms, "cast_ms": cast_ms, "tflops": flops / ((ms + cast_ms) * 1e-3) / 1e12,
             "note": "GEMMs plus torch's eager bf16 -> E4M3 operand preparation (dY, W^T, dY^T, x^T as "
