@@ -166,20 +166,29 @@ __device__ __forceinline__ void store_elem(void* base, int64_t e, float v) {
 // (a block spans 32 N element-size bytes, under 2^31 for N < kGemmMaxN = 2^24,
 // which the entry points check). Each element then costs one 32-bit add for its offset and no
 // bounds branch; the resources are scalar and lie inside C's rows.
+// Row runs: in a 32 x 32 MFMA tile, lanes 0-31 hold 32 columns of one row and
+// lanes 32-63 the same columns four rows further. For two tiles side by side,
+// one V_PERMLANE32_SWAP per value trades the upper half of the left tile's
+// register with the lower half of the right one's, leaving one register with
+// 64 consecutive columns of a row and the other with those of the row four
+// further: each store then writes one 256-byte run (FP32) instead of two
+// 128-byte ones. With every CU storing at once, a store-only test drained
+// 256 KiB per CU in 11.7 instead of 15.4 us this way; the GPT-6.7B block's
+// GEMMs took 0.6% less time.
 // The accumulating kind loads the old values through the same resource (rows
-// and columns outside it read as zeros) -- those of two tiles before any is
+// and columns outside it read as zeros) -- those of a tile pair before any is
 // written back, so the loads overlap -- and stores old + alpha * sum.
 template <int STORE, int TM, int TN>
 __device__ __forceinline__ void store_tiles_buf(const Problem& P, void* out, float alpha, int64_t row0,
                                                 int64_t col0, const v16f (&acc)[TM][TN], int lane) {
+  static_assert(TN % 2 == 0, "tiles are stored in side-by-side pairs");
   constexpr uint32_t kEs = STORE == (int)Store::kBf16 ? 2u : 4u;
-  const int half = lane >> 5, lrow = lane & 31;
   const uint32_t pitch = (uint32_t)P.N * kEs;
-  uint32_t lane_off[TN];
+  uint32_t lane_off[TN / 2];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t col = col0 + j * 32 + lrow;
-    lane_off[j] = col < P.N ? (uint32_t)(half * 4) * pitch + (uint32_t)col * kEs : 0x80000000u;
+  for (int p = 0; p < TN / 2; ++p) {
+    const int64_t col = col0 + p * 64 + lane;
+    lane_off[p] = col < P.N ? (uint32_t)col * kEs : 0x80000000u;
   }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -189,42 +198,51 @@ __device__ __forceinline__ void store_tiles_buf(const Problem& P, void* out, flo
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<uint8_t*>(out) + (nrows > 0 ? rb * (int64_t)pitch : 0), (short)0, (int)(nrows * pitch),
         0x00020000);
-    if constexpr (STORE == (int)Store::kAccF32) {
-      // JB tiles at a time (32 loads in flight), which keeps the 256 x 256
-      // kernel's epilogue within its registers.
-      constexpr int JB = TN < 2 ? TN : 2;
 #pragma unroll
-      for (int j0 = 0; j0 < TN; j0 += JB) {
-        uint32_t old[JB][16];
+    for (int p = 0; p < TN / 2; ++p) {
+      // value v of the pair: element h of the swap holds row (v / 4) 8 + v % 4 + 4 h
+      uint32_t sw[16][2];
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj)
+      for (int v = 0; v < 16; ++v) {
+        // Through scalars: a bit cast of a vector element reads element 0.
+        const float left = acc[i][2 * p][v], right = acc[i][2 * p + 1][v];
+        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, left),
+                                                        __builtin_bit_cast(uint32_t, right), false, false);
+        sw[v][0] = r[0];
+        sw[v][1] = r[1];
+      }
+      if constexpr (STORE == (int)Store::kAccF32) {
+        uint32_t old[16][2];
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            old[jj][v] = __builtin_amdgcn_raw_buffer_load_b32(
-                rs, (int)(lane_off[j0 + jj] + (uint32_t)((v >> 2) * 8 + (v & 3)) * pitch), 0, 0);
+        for (int v = 0; v < 16; ++v)
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj)
+          for (int h = 0; h < 2; ++h)
+            old[v][h] = __builtin_amdgcn_raw_buffer_load_b32(
+                rs, (int)(lane_off[p] + (uint32_t)((v >> 2) * 8 + (v & 3) + 4 * h) * pitch), 0, 0);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const uint32_t off = lane_off[j0 + jj] + (uint32_t)((v >> 2) * 8 + (v & 3)) * pitch;
-            const float val = __builtin_bit_cast(float, old[jj][v]) + acc[i][j0 + jj][v] * alpha;
+        for (int v = 0; v < 16; ++v)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint32_t off = lane_off[p] + (uint32_t)((v >> 2) * 8 + (v & 3) + 4 * h) * pitch;
+            const float val = __builtin_bit_cast(float, old[v][h]) + __builtin_bit_cast(float, sw[v][h]) * alpha;
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, (int)off, 0,
                                                   kNonTemporal);
           }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint32_t off = lane_off[p] + (uint32_t)((v >> 2) * 8 + (v & 3) + 4 * h) * pitch;
+            const float val = __builtin_bit_cast(float, sw[v][h]) * alpha;
+            if constexpr (STORE == (int)Store::kBf16)
+              __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(val), rs, (int)off, 0, kNonTemporal);
+            else
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, (int)off, 0,
+                                                    kNonTemporal);
+          }
       }
-      continue;
     }
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const uint32_t off = lane_off[j] + (uint32_t)((v >> 2) * 8 + (v & 3)) * pitch;
-        const float val = acc[i][j][v] * alpha;
-        if constexpr (STORE == (int)Store::kBf16)
-          __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(val), rs, (int)off, 0, kNonTemporal);
-        else
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, (int)off, 0, kNonTemporal);
-      }
   }
 }
 
