@@ -582,7 +582,7 @@ def cpu_oracle_full(config, linears=None):
 
 
 def cpu_baseline(config, budget_s):
-    """The CPU oracle timed on the GPU machine's host cores.
+    """The CPU oracle timed on this machine's host cores.
 
     * In full: the tiny single-linear config (256 tokens, 256 x 256) and the
       QKV linear of the GPT-345M block.
