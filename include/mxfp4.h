@@ -209,10 +209,11 @@ int64_t mx_gemm_f4_workspace_bytes(int64_t M, int64_t N, int64_t K);
 /*
  * Frees the workspace the library keeps for the current device and `stream`
  * (see mx_linear_backward), in stream order: the block is released after the
- * work already enqueued on `stream`, so calls enqueued before stay valid. The
- * next call on that stream allocates a new one. MX_OK also when the stream has
- * none; MX_ERR_HIP if the free fails. Not for a stream that is being captured
- * (MX_ERR_CAPTURE).
+ * work already enqueued on `stream`, so calls enqueued before stay valid, and
+ * its memory goes back to the device at the next synchronisation (of the
+ * stream, an event on it or the device). The next call on that stream
+ * allocates a new one. MX_OK also when the stream has none; MX_ERR_HIP if the
+ * free fails. Not for a stream that is being captured (MX_ERR_CAPTURE).
  */
 int mx_release_workspace(void* stream);
 

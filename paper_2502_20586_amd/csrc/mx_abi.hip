@@ -57,7 +57,11 @@ hipMemPool_t pool_for(int dev) {
     props.location.id = dev;
     hipMemPool_t pool = nullptr;
     if (hipMemPoolCreate(&pool, &props) == hipSuccess) {
-      uint64_t keep = ~0ull;
+      // Release threshold 0: a block freed in stream order (a workspace that
+      // grew, or mx_release_workspace) goes back to the device at the next
+      // synchronisation instead of staying reserved by the pool. Workspaces in
+      // use are not affected; they are kept, not freed, between calls.
+      uint64_t keep = 0;
       (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
       g_pools[dev] = pool;
     }

@@ -147,6 +147,33 @@ def test_release_workspace_between_gemms():
     mx.mx_release_workspace(fresh)                # a stream the library never saw
 
 
+def test_release_workspace_returns_memory():
+    """After mx_release_workspace and a synchronisation the device has the
+    workspace's memory back (the library's pool keeps no freed blocks)."""
+    torch = torch_gpu()
+    import paper_2502_20586_amd as mx
+    m, n, k = 65536, 8192, 8192
+    ws = mx.mx_gemm_f4_workspace_bytes(m, n, k)
+    assert ws > 300e6
+    a_codes = torch.zeros((m, k // 2), dtype=torch.uint8, device="cuda")
+    a_scales = torch.full((m, k // 32), 127, dtype=torch.uint8, device="cuda")
+    b_codes = torch.zeros((n, k // 2), dtype=torch.uint8, device="cuda")
+    b_scales = torch.full((n, k // 32), 127, dtype=torch.uint8, device="cuda")
+    c = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    note(f"workspace release: {ws / 1e6:.0f} MB")
+    mx.mx_gemm_f4(a_codes, a_scales, b_codes, b_scales, c, stream=s)
+    s.synchronize()
+    assert torch.count_nonzero(c).item() == 0
+    held = torch.cuda.mem_get_info()[0]
+    mx.mx_release_workspace(s)
+    s.synchronize()
+    torch.cuda.synchronize()
+    freed = torch.cuda.mem_get_info()[0] - held
+    assert freed >= 0.9 * ws, (freed, ws)
+
+
 def test_gemm_k_zero_and_empty():
     torch = torch_gpu()
     import paper_2502_20586_amd as mx
