@@ -24,7 +24,8 @@
  *   surface at the caller's next synchronisation of the stream.
  * - A call with an empty problem (a zero dimension) enqueues nothing and
  *   returns MX_OK; its pointers may then be NULL.
- * - Outputs are fully overwritten. Calls are thread-safe.
+ * - Outputs are fully overwritten (except what mx_linear_backward_ex is asked
+ *   to accumulate into). Calls are thread-safe.
  * - Graph capture: every call that enqueues work first asks whether `stream`
  *   is being captured into a HIP graph and, if so, returns MX_ERR_CAPTURE and
  *   enqueues nothing (these calls may allocate or free their workspace in
@@ -343,9 +344,10 @@ int64_t mx_linear_backward_ex_workspace_bytes(int64_t T, int64_t in_features, in
  * kernel's own execution. mx_profile_stop() waits for those events and fills `stats`
  * (up to `capacity` entries, one per kernel name; *count gets the number of
  * kernel names seen) with the number of launches, their summed GPU time and
- * their summed algorithmic work: bytes for the quantiser (2 bytes read and
- * 0.53125 bytes written per element), FLOPs (2 M N K) for the GEMM, bytes for
- * the split-K reduction. Tracing is process-wide; calls that overlap with
+ * their summed algorithmic work: bytes for the quantiser (2 bytes read per
+ * input element, once also when one pass writes two quantisations of it, and
+ * 0.53125 bytes written per quantised element), FLOPs (2 M N K) for the GEMM,
+ * bytes for the split-K reduction. Tracing is process-wide; calls that overlap with
  * mx_profile_stop() from another thread are not traced. mx_profile_stop()
  * consumes the session's records (a second call reports nothing). Returns MX_OK
  * or MX_ERR_HIP.
