@@ -105,6 +105,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed warm-up steps (default: enough to fill %.1f s, at least 20)" % WARMUP_S)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the MFMA-ceiling measurement (FP4 MFMAs from registers) beside the GEMM roofline")
     ap.add_argument("--no-baselines", action="store_true", help="skip the BF16 / FP8 GEMM baselines")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the framework-option variants (profiles of the headline step alone)")
@@ -1007,6 +1009,15 @@ def main():
         "step_ms_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "input_rotation": {"sets": len(sets), "input_bytes_per_set": set_bytes},
     }
+    if roof["bound"] == "mfma" and not args.no_ceiling:
+        # What the GEMM could reach at best: FP4 MFMAs back to back from
+        # registers on every CU, at the clock the chip holds under that load.
+        tf, ghz = mx.mx_measure_mfma_peak()
+        res["mfma_ceiling"] = {"tflops": tf, "clock_ghz": ghz,
+                               "what": "FP4 32x32x64 scaled MFMAs from registers, 16 independent tiles per wave, "
+                                       "one 4-wave workgroup per CU, no memory traffic"}
+        roof["frac_of_mfma_ceiling"] = roof["achieved"] / tf
+        print(f"[bench] MFMA ceiling {tf:.0f} TFLOP/s at {ghz:.2f} GHz", file=sys.stderr, flush=True)
     if not args.no_variants:
         print("[bench] framework option variants", file=sys.stderr, flush=True)
         res["variants"] = variants(torch, mx, sets, g, max(10, args.steps // 2), min(args.warmup, 10))

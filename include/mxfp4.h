@@ -352,6 +352,20 @@ int64_t mx_linear_backward_ex_workspace_bytes(int64_t T, int64_t in_features, in
  * consumes the session's records (a second call reports nothing). Returns MX_OK
  * or MX_ERR_HIP.
  */
+/*
+ * The attainable MFMA rate, for the GEMM's roofline: every CU runs one
+ * workgroup whose four waves issue `rounds` rounds of 16 independent FP4
+ * V_MFMA_SCALE_F32_32X32X64_F8F6F4 from registers (no memory traffic), timed
+ * over 50 launches after about 0.3 s of warm-up launches, on a stream of the
+ * library's own; the call synchronises and is not for use during other work.
+ * *tflops gets the dense FP4 rate achieved and *clock_ghz the shader clock it
+ * ran at (s_memtime cycles of one wave over the launch time): under full MFMA
+ * load the chip holds a clock below the nominal 2.4 GHz, so this is what a
+ * GEMM can reach at best. rounds in [1, 2^20] (MX_ERR_SHAPE otherwise; 2000
+ * gives launches of about half a millisecond).
+ */
+int mx_measure_mfma_peak(int rounds, double* tflops, double* clock_ghz);
+
 typedef struct mx_kernel_stat {
   char name[48];        /* kernel name, e.g. "quant_g64", "gemm_128x128" */
   int64_t launches;

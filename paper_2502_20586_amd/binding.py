@@ -96,6 +96,8 @@ def load_library():
     lib.mx_profile_start.argtypes = []
     lib.mx_profile_stop.restype = ci
     lib.mx_profile_stop.argtypes = [ctypes.POINTER(KernelStat), ci, ctypes.POINTER(ci)]
+    lib.mx_measure_mfma_peak.restype = ci
+    lib.mx_measure_mfma_peak.argtypes = [ci, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     _LIB = lib
     return lib
 
@@ -310,3 +312,11 @@ def mx_profile_stop():
         out[s.name.decode()] = {"launches": int(s.launches), "total_ms": float(s.total_ms),
                                 "work": float(s.work), "work_is_flops": bool(s.work_is_flops)}
     return out
+
+
+def mx_measure_mfma_peak(rounds=2000):
+    """(TFLOP/s, clock GHz) of FP4 MFMAs issued back to back from registers on every CU:
+    the rate the GEMM can reach at best. Synchronises; takes about half a second."""
+    tf, ghz = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(load_library().mx_measure_mfma_peak(rounds, ctypes.byref(tf), ctypes.byref(ghz)))
+    return tf.value, ghz.value

@@ -423,6 +423,14 @@ int64_t gemm_f4_layout(const mx::GemmArgs& g, bool* kt, int64_t* partial_bytes, 
 
 extern "C" {
 
+int mx_measure_mfma_peak(int rounds, double* tflops, double* clock_ghz) {
+  if (!tflops || !clock_ghz) return MX_ERR_NULL;
+  if (rounds < 1 || rounds > (1 << 20)) return MX_ERR_SHAPE;
+  int st = check_device();
+  if (st != MX_OK) return st;
+  return mx::measure_mfma_peak(rounds, tflops, clock_ghz) ? MX_ERR_HIP : MX_OK;
+}
+
 int64_t mx_gemm_f4_workspace_bytes(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || K < 0 || K % 32 != 0 || N >= mx::kGemmMaxN) return 0;
   const mx::GemmArgs g{nullptr, nullptr, nullptr, nullptr, nullptr, M, N, K, 1.0f, false};

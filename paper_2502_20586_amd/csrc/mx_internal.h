@@ -95,6 +95,11 @@ int launch_ktile_repack(const uint8_t* codes, const uint8_t* scales, uint8_t* kc
 int64_t gemm_workspace_bytes(const GemmArgs* probs, int count);
 int launch_gemm(const GemmArgs* probs, int count, float* partial_ws, hipStream_t stream);
 
+// The attainable MFMA rate (mx_measure_mfma_peak): FP4 MFMAs from registers
+// on every CU, timed over 50 launches after a 0.3 s warm-up on a stream of its
+// own; synchronises. Returns 0, or -1 if a HIP call failed.
+int measure_mfma_peak(int rounds, double* tflops, double* clock_ghz);
+
 // Tracing (mx_profile_start / mx_profile_stop): while tracing is on, a
 // TraceScope holds a pair of HIP events for one launch; the launch passes them
 // to hipExtLaunchKernel, which records them at the kernel's start and end

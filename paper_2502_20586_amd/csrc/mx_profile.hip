@@ -59,6 +59,104 @@ TraceScope::TraceScope(const char* name, double work, bool flops) {
   stop_ = r.stop;
 }
 
+// ---------------------------------------------------------------------------
+// Attainable MFMA rate. Each wave issues `rounds` rounds of 16 independent
+// V_MFMA_SCALE_F32_32X32X64_F8F6F4 (FP4 x FP4; the 16 accumulator tiles of
+// one 256 x 256 GEMM wave) from registers, with no memory traffic, so the
+// launch runs at the rate the matrix cores sustain under full load -- at the
+// clock the chip holds under that load, which is below the nominal one.
+constexpr int kPeakTiles = 16;
+// External linkage, so the device compiler keeps the stores (and with them the
+// MFMAs) although no device code reads these back.
+__device__ float g_peak_sink[kPeakTiles * 16];       // one sum per lane of block 0
+__device__ uint64_t g_peak_cycles[2];                 // s_memtime span of block 0, wave 0
+
+namespace {
+typedef float v16f_p __attribute__((ext_vector_type(16)));
+typedef int v8i_p __attribute__((ext_vector_type(8)));
+
+__global__ __launch_bounds__(256, 1) void mfma_peak_kernel(int rounds, int salt) {
+  v16f_p acc[kPeakTiles];
+#pragma unroll
+  for (int t = 0; t < kPeakTiles; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
+  // Four A and four B fragments of pseudo-random FP4 codes (a multiplicative
+  // hash of lane, salt and word), combined as a GEMM wave combines its
+  // fragments: every MFMA sees other operand bits than the one before, as in
+  // a real K loop (constant operands would draw less power and let the clock
+  // run higher than any GEMM could).
+  const uint32_t lane = threadIdx.x & 63;
+  v8i_p a[4], b[4];
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const uint32_t h = (lane * 8u + w + 0x9E3779B9u * (uint32_t)(salt + 16 * f + 1)) * 0x85EBCA6Bu;
+      a[f][w] = w < 4 ? (int)(h ^ (h >> 13)) : 0;
+      const uint32_t k = (lane * 8u + w + 0xC2B2AE35u * (uint32_t)(salt + 16 * f + 7)) * 0x27D4EB2Fu;
+      b[f][w] = w < 4 ? (int)(k ^ (k >> 15)) : 0;
+    }
+  const uint64_t t0 = __builtin_amdgcn_s_memtime();
+  for (int r = 0; r < rounds; ++r) {
+#pragma unroll
+    for (int t = 0; t < kPeakTiles; ++t)
+      acc[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[t >> 2], b[t & 3], acc[t], 4, 4, 0, 120, 0, 121);
+  }
+  const uint64_t t1 = __builtin_amdgcn_s_memtime();
+  float sum = 0.0f;                                    // element 0 of every tile keeps its MFMA chain
+#pragma unroll
+  for (int t = 0; t < kPeakTiles; ++t) sum += acc[t][0];
+  // Block 0 writes its sums (plain vector stores).
+  if (blockIdx.x == 0 && threadIdx.x < kPeakTiles * 16) g_peak_sink[threadIdx.x] = sum;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    g_peak_cycles[0] = t0;
+    g_peak_cycles[1] = t1;
+  }
+}
+}  // namespace
+
+int measure_mfma_peak(int rounds, double* tflops, double* clock_ghz) {
+  int dev = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return -1;
+  const int blocks = prop.multiProcessorCount;          // one 4-wave workgroup per CU (512 registers a lane)
+  hipStream_t s = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return -1;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int status = -1;
+  if (hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess) {
+    // Warm-up of about 0.3 s: the clocks settle under sustained load.
+    bool ok = true;
+    for (int i = 0; ok && i < 600; ++i) {
+      hipLaunchKernelGGL(mfma_peak_kernel, dim3(blocks), dim3(256), 0, s, rounds, i);
+      ok = hipGetLastError() == hipSuccess;
+    }
+    const int reps = 50;
+    ok = ok && hipEventRecord(e0, s) == hipSuccess;
+    for (int i = 0; ok && i < reps; ++i) {
+      hipLaunchKernelGGL(mfma_peak_kernel, dim3(blocks), dim3(256), 0, s, rounds, i);
+      ok = hipGetLastError() == hipSuccess;
+    }
+    ok = ok && hipEventRecord(e1, s) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
+    float ms = 0.0f;
+    uint64_t cyc[2] = {0, 0};
+    ok = ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess &&
+         hipMemcpyFromSymbol(cyc, HIP_SYMBOL(g_peak_cycles), sizeof(cyc), 0, hipMemcpyDeviceToHost) == hipSuccess;
+    if (ok && ms > 0.0f) {
+      const double per_launch_s = ms * 1e-3 / reps;
+      const double flops = (double)blocks * 4 * rounds * kPeakTiles * (32.0 * 32 * 64 * 2);
+      *tflops = flops / per_launch_s / 1e12;
+      *clock_ghz = (double)(cyc[1] - cyc[0]) / per_launch_s / 1e9;
+      status = 0;
+    }
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipStreamDestroy(s);
+  return status;
+}
+
 }  // namespace mx
 
 extern "C" {

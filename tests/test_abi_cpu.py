@@ -108,6 +108,16 @@ def test_quantize_pair_validation():
     assert f(None, None, None, None, None, 0, 128, 64, 0, 2, RHT_SR, None) == 0       # empty
 
 
+def test_measure_mfma_peak_validation():
+    """Arguments are checked before any device work: NULL outputs, then the round count."""
+    import ctypes
+    lib = _lib()
+    a, b = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    assert lib.mx_measure_mfma_peak(2000, None, ctypes.byref(b)) == -1          # MX_ERR_NULL
+    assert lib.mx_measure_mfma_peak(0, ctypes.byref(a), ctypes.byref(b)) == -3  # MX_ERR_SHAPE
+    assert lib.mx_measure_mfma_peak((1 << 20) + 1, ctypes.byref(a), ctypes.byref(b)) == -3
+
+
 def test_gemm_workspace_bytes():
     """mx_gemm_f4_workspace_bytes: 0 for invalid or empty sizes; for K % 128 == 0 at
     least the K-tiled copies of both operands (0.53125 byte per element, each part

@@ -147,6 +147,29 @@ def test_release_workspace_between_gemms():
     mx.mx_release_workspace(fresh)                # a stream the library never saw
 
 
+def test_mfma_ceiling_is_plausible_and_above_the_gemm():
+    """mx_measure_mfma_peak: FP4 MFMAs from registers run below the published
+    10.1 PFLOP/s (the clock drops under full MFMA load) but well above what the
+    GEMM kernel reaches, and at a clock under the nominal 2.4 GHz."""
+    torch = torch_gpu()
+    import paper_2502_20586_amd as mx
+    note("mfma ceiling")
+    tf, ghz = mx.mx_measure_mfma_peak(2000)
+    assert 3000 < tf <= 10100 * 1.02, tf
+    assert 0.8 < ghz < 2.5, ghz
+    rng = np.random.default_rng(21)
+    m = n = k = 8192
+    a, b = _rand_mx(rng, m, k), _rand_mx(rng, n, k)
+    ops = [to_dev_u8(pack_codes(a[0])), to_dev_u8(a[1]), to_dev_u8(pack_codes(b[0])), to_dev_u8(b[1])]
+    c = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    mx.mx_gemm_f4(*ops, c)
+    mx.mx_profile_start()
+    mx.mx_gemm_f4(*ops, c)
+    st = mx.mx_profile_stop()["gemm_256x256"]
+    gemm_tf = st["work"] / (st["total_ms"] * 1e-3) / 1e12
+    assert gemm_tf < tf, (gemm_tf, tf)
+
+
 def test_release_workspace_returns_memory():
     """After mx_release_workspace and a synchronisation the device has the
     workspace's memory back (the library's pool keeps no freed blocks)."""
