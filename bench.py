@@ -152,6 +152,24 @@ class Layer:
         return 2 * self.t * self.fout + self.fin * self.fout + self.fin * self.t
 
 
+def gemm_attainable(layers, gemm_ms_per_step):
+    """The GEMMs' attainable time per step: for each backward GEMM (dX: M, N, K =
+    T, in, out; dW: out, in, T) the larger of its MFMA time at the MXFP4 peak and
+    its HBM time at 8 TB/s for its algorithmic bytes (MXFP4 operands at 0.53125 B
+    per element, FP32 output written once), summed over the step; `frac` is that
+    over the measured GEMM time."""
+    us, n_hbm, n_mfma = 0.0, 0, 0
+    for L in layers:
+        for m, n, k in ((L.t, L.fin, L.fout), (L.fout, L.fin, L.t)):
+            t_mfma = 2.0 * m * n * k / (MXFP4_PEAK_TFLOPS * 1e12)
+            t_hbm = ((m + n) * k * 0.53125 + 4.0 * m * n) / (HBM_PEAK_GBS * 1e9)
+            us += max(t_mfma, t_hbm) * 1e6
+            n_hbm += t_hbm > t_mfma
+            n_mfma += t_hbm <= t_mfma
+    return {"us_per_step": us, "frac": us / (gemm_ms_per_step * 1e3), "mfma_bound_gemms": n_mfma,
+            "hbm_bound_gemms": n_hbm}
+
+
 def step(mx, layers, g):
     for L in layers:
         mx.mx_linear_backward(L.dy, L.x, L.w, L.dx, L.dw, g, SEED)
@@ -998,6 +1016,7 @@ def main():
         "quantize_ms_per_step": quant_ms / args.steps,
         "gemm_ms_per_step": gemm_ms / args.steps,
         "gemm_tflops": flops * args.steps / (gemm_ms * 1e-3) / 1e12,
+        "gemm_attainable": gemm_attainable(layers, gemm_ms / args.steps),
         "mfma_peak_frac": value / MXFP4_PEAK_TFLOPS,
         "roofline": roof,
         "quantize_roofline": roofline_of(config, prof, qk, args.steps) if qk else None,
@@ -1055,8 +1074,10 @@ def main():
         ms2 = e0.elapsed_time(e1) / n2
         flops2 = sum(L.flops() for L in layers2)
         prof2, kern2 = traced(torch, mx, sets2, cfg2["g"][0], n2)
+        gemm_ms2 = sum(v["total_ms"] for k, v in prof2.items() if k.startswith("gemm") or k == "splitk_reduce") / n2
         sec = {"workload": f"{SECONDARY_CONFIG}_block_backward", "steps": n2, "ms_per_step": ms2,
-               "tflops": flops2 / (ms2 * 1e-3) / 1e12, "kernels": kern2}
+               "tflops": flops2 / (ms2 * 1e-3) / 1e12, "kernels": kern2,
+               "gemm_attainable": gemm_attainable(layers2, gemm_ms2)}
         if not args.no_baselines:
             sec["baselines"] = gemm_baselines(torch, layers2)
             sec["speedups"] = {f"vs_{k}": v["ms_per_step"] / ms2 for k, v in sec["baselines"].items()
