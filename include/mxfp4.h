@@ -352,6 +352,17 @@ int64_t mx_linear_backward_ex_workspace_bytes(int64_t T, int64_t in_features, in
  * consumes the session's records (a second call reports nothing). Returns MX_OK
  * or MX_ERR_HIP.
  */
+typedef struct mx_kernel_stat {
+  char name[48];        /* kernel name, e.g. "quant_g64", "gemm_128x128" */
+  int64_t launches;
+  double total_ms;      /* summed event-to-event time of its launches */
+  double work;          /* summed algorithmic work */
+  int work_is_flops;    /* 1: work is FLOPs, 0: work is bytes */
+} mx_kernel_stat;
+
+int mx_profile_start(void);
+int mx_profile_stop(mx_kernel_stat* stats, int capacity, int* count);
+
 /*
  * The attainable MFMA rate, for the GEMM's roofline: every CU runs one
  * workgroup whose four waves issue `rounds` rounds of 16 independent FP4
@@ -365,17 +376,6 @@ int64_t mx_linear_backward_ex_workspace_bytes(int64_t T, int64_t in_features, in
  * gives launches of about half a millisecond).
  */
 int mx_measure_mfma_peak(int rounds, double* tflops, double* clock_ghz);
-
-typedef struct mx_kernel_stat {
-  char name[48];        /* kernel name, e.g. "quant_g64", "gemm_128x128" */
-  int64_t launches;
-  double total_ms;      /* summed event-to-event time of its launches */
-  double work;          /* summed algorithmic work */
-  int work_is_flops;    /* 1: work is FLOPs, 0: work is bytes */
-} mx_kernel_stat;
-
-int mx_profile_start(void);
-int mx_profile_stop(mx_kernel_stat* stats, int capacity, int* count);
 
 #ifdef __cplusplus
 }
