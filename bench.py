@@ -608,60 +608,69 @@ def cpu_baseline(config, budget_s):
       QKV linear of the GPT-345M block.
     * Sampled, for the headline block (whose oracle step runs for most of an
       hour): per linear, the oracle quantises whole rows of each of the four
-      operands -- the first 64 logical rows of dY and dY^T, the first 256 of W^T
-      and x^T (quantisation is row-local, so a row sample is exact work) -- and
-      multiplies the sampled rows of both GEMMs in FP64. The step time is the
-      measured per-element quantise time times the step's elements plus the
-      measured per-FLOP GEMM time times its FLOPs. The skinny sampled GEMMs run
-      BLAS below its full-size rate, so this estimate errs towards a slower
+      operands -- 64 logical rows of dY and dY^T, 256 of W^T and x^T per pass
+      (quantisation is row-local, so a row sample is exact work) -- and
+      multiplies the sampled rows of both GEMMs in FP64. Passes take the next
+      rows (wrapping around) until about `budget_s` seconds of CPU work have
+      run, the two full runs included. The step time is the measured
+      per-element quantise time times the step's elements plus the measured
+      per-FLOP GEMM time times its FLOPs. The skinny sampled GEMMs run BLAS
+      below its full-size rate, so this estimate errs towards a slower
       oracle."""
     import oracle
     import workloads
     threads = _blas_threads()
+    start = time.perf_counter()
     full = {"tiny": cpu_oracle_full("tiny"), "gpt345m_qkv": cpu_oracle_full("gpt345m", ["qkv"])}
     cfg = workloads.CONFIGS[config]
     t, g = cfg["tokens"], cfg["g"][0]
-    q_elems_total, flops_total = 0, 0
+    q_elems_total = sum(2 * t * fout + fin * fout + fin * t for _, fin, fout in cfg["linears"])
+    flops_total = sum(4 * t * fin * fout for _, fin, fout in cfg["linears"])
     q_time, q_elems, g_time, g_flops = 0.0, 0, 0.0, 0
-    start = time.perf_counter()
     rows_a, rows_b = 64, 256
-    sampled = []
-    for name, fin, fout in cfg["linears"]:
-        q_elems_total += 2 * t * fout + fin * fout + fin * t
-        flops_total += 4 * t * fin * fout
-        if time.perf_counter() - start > budget_s:
-            continue
-        dy, x, w = workloads.linear_inputs(config, name)
-        # Logical rows of the four operands: dY [T, out], W^T [in, out],
-        # dY^T [out, T], x^T [in, T]; a row of a transposed operand is a column
-        # of the stored matrix.
-        ops = [(dy[:rows_a], 0), (np.ascontiguousarray(w[:, :rows_b].T), 1),
-               (np.ascontiguousarray(dy[:, :rows_a].T), 2), (np.ascontiguousarray(x[:, :rows_b].T), 3)]
-        qs = []
-        for bits, i in ops:
-            ids = np.arange(bits.shape[0])
-            t0 = time.perf_counter()
-            qs.append(oracle.quantize_rht_sr(bits, g, SEED ^ i, row_ids=ids))
-            q_time += time.perf_counter() - t0
-            q_elems += bits.size
-        for a, b in ((qs[0], qs[1]), (qs[2], qs[3])):
-            t0 = time.perf_counter()
-            oracle.gemm_f64(a[0], a[1], b[0], b[1])
-            g_time += time.perf_counter() - t0
-            g_flops += 2 * a[0].shape[0] * b[0].shape[0] * a[0].shape[1]
-        sampled.append(name)
+    inputs = {}
+    passes = 0
+    while passes == 0 or time.perf_counter() - start < budget_s:
+        for name, fin, fout in cfg["linears"]:
+            if name not in inputs:
+                inputs[name] = workloads.linear_inputs(config, name)
+            dy, x, w = inputs[name]
+            # Logical rows of the four operands: dY [T, out], W^T [in, out],
+            # dY^T [out, T], x^T [in, T]; a row of a transposed operand is a
+            # column of the stored matrix. Pass p takes rows p * rows_a ...
+            # (rows_a of dY and dY^T) and p * rows_b ... (rows_b of W^T, x^T).
+            ra = (passes * rows_a) % (min(t, fout) - rows_a + 1)
+            rb = (passes * rows_b) % (fin - rows_b + 1)
+            ops = [(dy[ra:ra + rows_a], ra, 0), (np.ascontiguousarray(w[:, rb:rb + rows_b].T), rb, 1),
+                   (np.ascontiguousarray(dy[:, ra:ra + rows_a].T), ra, 2),
+                   (np.ascontiguousarray(x[:, rb:rb + rows_b].T), rb, 3)]
+            qs = []
+            for bits, r0, i in ops:
+                ids = np.arange(r0, r0 + bits.shape[0])
+                t0 = time.perf_counter()
+                qs.append(oracle.quantize_rht_sr(bits, g, SEED ^ i, row_ids=ids))
+                q_time += time.perf_counter() - t0
+                q_elems += bits.size
+            for a, b in ((qs[0], qs[1]), (qs[2], qs[3])):
+                t0 = time.perf_counter()
+                oracle.gemm_f64(a[0], a[1], b[0], b[1])
+                g_time += time.perf_counter() - t0
+                g_flops += 2 * a[0].shape[0] * b[0].shape[0] * a[0].shape[1]
+        passes += 1
+    del inputs
     est_s = q_elems_total * (q_time / q_elems) + flops_total * (g_time / g_flops)
+    names = ", ".join(n for n, _, _ in cfg["linears"])
     return {
         "value": flops_total / est_s / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
         "host_cpus": os.cpu_count(),
-        "sample": (f"{config} block step, sampled: the oracle quantised {q_elems} elements (whole logical rows: "
-                   f"the first {rows_a} of dY and dY^T, the first {rows_b} of W^T and x^T, of the linears "
-                   f"{', '.join(sampled)}) and ran {g_flops:.3g} FLOPs of the FP64 GEMMs on those rows; step time "
-                   f"= per-element quantise time x {q_elems_total} elements + per-FLOP GEMM time x "
+        "sample": (f"{config} block step, sampled: in {passes} passes over the linears {names}, the oracle "
+                   f"quantised {q_elems} elements (whole logical rows, per pass {rows_a} of dY and dY^T and "
+                   f"{rows_b} of W^T and x^T) and ran {g_flops:.3g} FLOPs of the FP64 GEMMs on those rows; step "
+                   f"time = per-element quantise time x {q_elems_total} elements + per-FLOP GEMM time x "
                    f"{flops_total:.4g} FLOPs = {est_s:.0f} s. Quantiser single-threaded numpy, GEMM BLAS on "
-                   f"{threads} threads"),
+                   f"{threads} threads; {time.perf_counter() - start:.1f} s of CPU work with the full runs"),
         "quant_elems_per_s": q_elems / q_time, "gemm_flops_per_s": g_flops / g_time, "est_step_s": est_s,
-        "full_runs": full,
+        "passes": passes, "full_runs": full,
     }
 
 
