@@ -668,7 +668,8 @@ def cpu_baseline(config, budget_s):
                    f"{rows_b} of W^T and x^T) and ran {g_flops:.3g} FLOPs of the FP64 GEMMs on those rows; step "
                    f"time = per-element quantise time x {q_elems_total} elements + per-FLOP GEMM time x "
                    f"{flops_total:.4g} FLOPs = {est_s:.0f} s. Quantiser single-threaded numpy, GEMM BLAS on "
-                   f"{threads} threads; {time.perf_counter() - start:.1f} s of CPU work with the full runs"),
+                   f"{threads} threads; {time.perf_counter() - start:.1f} s in all, the full runs and the generation "
+                   f"of the sampled linears' inputs included"),
         "quant_elems_per_s": q_elems / q_time, "gemm_flops_per_s": g_flops / g_time, "est_step_s": est_s,
         "passes": passes, "full_runs": full,
     }
