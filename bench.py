@@ -125,7 +125,8 @@ def parse():
                     help="variance of the SR inner-product estimator with and without the RHT (the figure of "
                          "Sec. 3.2) and the flush-to-zero statistic, through the HIP path")
     ap.add_argument("--co-schedule", action="store_true",
-                    help="two independent GPT-6.7B block backwards on one stream and on two streams")
+                    help="two independent block backwards (--config, default GPT-6.7B) on one stream and on two "
+                         "streams")
     ap.add_argument("--configs", action="store_true",
                     help="instead of the step: GPT-1.3B (every g) and GPT-6.7B block backward end to end, "
                          "with BF16 / FP8 GEMM baselines on the same shapes")
@@ -444,17 +445,21 @@ def rht_variance(torch, mx, draws=64, oracle_rows=256):
     return {"variance": rows, "flush_to_zero": flush}
 
 
-def co_schedule(torch, mx, reps=10, rounds=3):
-    """Two independent GPT-6.7B block backwards (two micro-batches' worth of
-    inputs and outputs), run back to back on one stream and concurrently on two
-    streams of the same priority, the second stream taking the linears in
-    reverse order so that its quantiser launches tend to meet the first
-    stream's GEMM launches. A GEMM workgroup holds a whole SIMD's registers (one
-    wave per SIMD), so the two kernels cannot share a CU: any gain comes from
-    the hardware filling CUs that one launch leaves idle (launch tails, the
-    tiles' synchronised store bursts) with the other stream's work."""
-    _, layers = load_layers(torch, "gpt6.7b")
-    g = 64
+def co_schedule(torch, mx, config="gpt6.7b", reps=None, rounds=3):
+    """Two independent block backwards (two micro-batches' worth of inputs and
+    outputs; GPT-6.7B unless --config names another block), run back to back
+    on one stream and concurrently on two streams of the same priority, the
+    second stream taking the linears in reverse order so that its quantiser
+    launches tend to meet the first stream's GEMM launches. A 256 x 256 GEMM
+    workgroup holds a whole SIMD's registers (one wave per SIMD), so at
+    GPT-6.7B the two kernels cannot share a CU: any gain comes from the
+    hardware filling CUs that one launch leaves idle (launch tails, the tiles'
+    synchronised store bursts) with the other stream's work. Smaller blocks
+    run the 128 x 128 kernel (two workgroups per CU) and shorter launches."""
+    cfg, layers = load_layers(torch, config)
+    g = cfg["g"][0]
+    if reps is None:   # about 40 ms or more per timed run
+        reps = 10 if config == "gpt6.7b" else 100
     other = []
     for L in layers:
         c = Layer.__new__(Layer)
@@ -483,7 +488,7 @@ def co_schedule(torch, mx, reps=10, rounds=3):
     cases = {"one_stream": (layers + other, []), "two_streams_same_order": (layers, other),
              "two_streams_reversed": (layers, other[::-1])}
     for a, b in cases.values():
-        run(a, b, 3)
+        run(a, b, max(3, reps // 2))
     times = {k: [] for k in cases}
     for _ in range(rounds):
         for k, (a, b) in cases.items():
@@ -491,7 +496,9 @@ def co_schedule(torch, mx, reps=10, rounds=3):
     med = {k: sorted(v)[len(v) // 2] for k, v in times.items()}
     for s in (sa, sb):
         mx.mx_release_workspace(s)
-    return {"workload": "two gpt6.7b block backwards (T=16384, hidden 4096, g=64), independent inputs",
+    hidden = layers[0].fin
+    return {"workload": f"two {config} block backwards (T={cfg['tokens']}, hidden {hidden}, g={g}), "
+                        "independent inputs",
             "ms_per_two_blocks": {k: round(v, 4) for k, v in med.items()},
             "all_rounds_ms": {k: [round(t, 4) for t in v] for k, v in times.items()},
             "gain_vs_one_stream": {k: round(med["one_stream"] / v - 1, 4) for k, v in med.items()
@@ -972,7 +979,7 @@ def main():
         print(json.dumps({"rht_variance": rht_variance(torch, mx)}))
         return
     if args.co_schedule:
-        print(json.dumps({"co_schedule": co_schedule(torch, mx)}))
+        print(json.dumps({"co_schedule": co_schedule(torch, mx, args.config)}))
         return
     config = args.config
     t0 = time.perf_counter()
